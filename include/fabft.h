@@ -1,0 +1,151 @@
+/*
+ * fabft.h - C ABI of the Flash-ABFT attention forward library (libfabft.so)
+ * for AMD Instinct MI355X (gfx950).
+ *
+ * Flash-ABFT (arXiv 2507.16676) computes attention O = softmax(scale*Q K^T) V
+ * (Eq. 1) with the one-pass FlashAttention-2 recurrence and, fused into the
+ * same pass, a predicted output checksum per query row (Algorithm 3):
+ *
+ *   c <- c * exp(m_old - m_new) + sumrow_k(V) * exp(s_k - m_new)
+ *
+ * where sumrow_k(V) is the sum of row k of V (Eq. 4). After the last key
+ * block, pred = c / l is the predicted sum of the output row (Eq. 8) and is
+ * compared with the actual row sum of O: one check per query row.
+ *
+ * Conventions for every entry point:
+ *  - q, k, v, o are DEVICE pointers to bfloat16 bit patterns (uint16),
+ *    contiguous row-major [B, H, Lq, d] (q, o) and [B, H, Lk, d] (k, v),
+ *    16-byte aligned. resid is fp32 [B, H, Lq], flags is uint8 [B, H, Lq],
+ *    pred/actual (when given) fp32 [B, H, Lq]; all device pointers.
+ *  - The caller owns every buffer. The library allocates nothing and keeps
+ *    only a stream and the detection threshold as process-global state
+ *    (setters are not thread-safe).
+ *  - d must be 64 or 128. B, H, Lq, Lk >= 1. scale must be finite and >= 0.
+ *  - causal != 0 keeps key k for query i iff k <= i + (Lk - Lq)
+ *    (bottom-right aligned; the plain lower triangle when Lq == Lk). A query
+ *    row with no visible key gets O = 0, pred = actual = resid = 0, flag 0.
+ *  - Arguments are validated before anything is launched; on error a
+ *    negative status is returned and nothing is written. Launches are
+ *    asynchronous on the library stream; FABFT_E_LAUNCH reports a launch
+ *    failure seen by hipGetLastError; device faults surface at the caller's
+ *    next synchronisation. Production entry points never synchronise.
+ *  - Computation: bf16 MFMA with fp32 accumulation for Q K^T and P V; the
+ *    softmax weights fed to P V are rounded to bf16 (p~), and the checksum
+ *    uses exactly those p~; l, c, the row sums and the residual are fp32.
+ *  - Results are bitwise deterministic run to run for fixed inputs.
+ */
+#ifndef FABFT_H
+#define FABFT_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  FABFT_OK = 0,
+  FABFT_E_NULL = -1,     /* a required pointer is NULL */
+  FABFT_E_SHAPE = -2,    /* B, H, Lq or Lk < 1, or the grid is too large */
+  FABFT_E_HEADDIM = -3,  /* d is not 64 or 128 */
+  FABFT_E_ALIGN = -4,    /* q, k, v or o not 16-byte aligned */
+  FABFT_E_LAUNCH = -5,   /* the kernel launch failed */
+  FABFT_E_SCALE = -6,    /* scale negative, NaN or infinite */
+  FABFT_E_FAULT = -7,    /* fault descriptor out of range */
+  FABFT_E_THRESHOLD = -8 /* threshold negative or NaN */
+};
+
+/* Detection flags, one byte per query row. */
+enum {
+  FABFT_FLAG_RESID = 1,    /* |pred - actual| > tau_rel * M + tau_abs, where
+                              M = sum_j |O_ij| + |pred| */
+  FABFT_FLAG_NONFINITE = 2 /* the residual is NaN or infinite */
+};
+
+/*
+ * Flash-ABFT attention forward (Algorithm 3; Eq. 8 per query row).
+ * Writes O (bf16, round-to-nearest-even of the fp32 normalised output),
+ * resid = pred - actual (fp32) and flags for every query row, where
+ * actual = sum_j O_ij is taken from the fp32 output before bf16 rounding.
+ */
+int fabft_attn_fwd(const void* q, const void* k, const void* v, void* o,
+                   float* resid, uint8_t* flags,
+                   int B, int H, int Lq, int Lk, int d, int causal,
+                   float scale);
+
+/*
+ * The same attention without the checksum (Algorithm 2): identical tiling,
+ * identical O bit for bit; only the sumrow, c-update and epilogue check are
+ * compiled out. Used to measure the checksum's cost.
+ */
+int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v,
+                           void* o, int B, int H, int Lq, int Lk, int d,
+                           int causal, float scale);
+
+/* Stream for all subsequent launches (a hipStream_t; NULL = null stream). */
+void fabft_set_stream(void* hip_stream);
+
+/*
+ * Detection threshold: a row is flagged when NOT |r| <= tau_rel*M + tau_abs
+ * (so a NaN residual is flagged). Defaults: tau_rel = 2^-12, tau_abs = 0.
+ * Returns FABFT_E_THRESHOLD (and keeps the old values) for negative or NaN.
+ */
+int fabft_set_threshold(float tau_rel, float tau_abs);
+void fabft_get_threshold(float* tau_rel, float* tau_abs);
+
+/* Number of keys per key tile of the kernel for head dimension d (the unit
+ * of fabft_fault.tile at the O site), or FABFT_E_HEADDIM. */
+int fabft_key_tile(int d);
+
+/* Number of query rows per workgroup (the unit of fabft_fault.tile at the
+ * V site). */
+int fabft_query_tile(void);
+
+/* Fault sites for the injection path (where a single bit is flipped). */
+enum {
+  FABFT_SITE_NONE = 0, /* no fault: debug run returning pred and actual */
+  FABFT_SITE_S = 1,    /* fp32 score s_ik after Q K^T, before the row max */
+  FABFT_SITE_P = 2,    /* bf16 weight p~_ik after the checksum has read it,
+                          before the P V product */
+  FABFT_SITE_O = 3,    /* fp32 output accumulator o_ij right after the
+                          P V product of key tile `tile` */
+  FABFT_SITE_V = 4     /* bf16 V_kj in the on-chip copy of one workgroup,
+                          after sumrow_k(V) was taken, before the P V product
+                          reads it; every query row of that workgroup that
+                          sees key k reads the flipped value */
+};
+
+/*
+ * One single-bit fault. b, h select the head. For S and P: row = query i,
+ * col = key k (must be visible to i). For O: row = query i, col = output
+ * column j, tile = key tile index t (the fault lands after tile t; t must be
+ * a tile that row i processes: t*key_tile <= last visible key of i). For V:
+ * row = key k, col = column j, tile = query tile (rows tile*query_tile ..
+ * tile*query_tile + query_tile - 1) whose workgroup holds the flipped copy.
+ * bit: 0..31 for fp32 sites (S, O), 0..15 for bf16 sites (P, V).
+ */
+typedef struct {
+  int site, b, h, row, col, tile, bit;
+} fabft_fault;
+
+/*
+ * Debug / fault-injection variant of fabft_attn_fwd (a separate kernel
+ * instantiation; the production kernels carry no injection code).
+ * f may be NULL (same as site NONE). pred and actual may be NULL; when
+ * given, they receive c/l and sum_j O_ij per row (fp32 [B, H, Lq]).
+ * Returns FABFT_E_FAULT if the descriptor is out of range. Asynchronous.
+ */
+int fabft_attn_fwd_inject(const void* q, const void* k, const void* v,
+                          void* o, float* resid, uint8_t* flags,
+                          int B, int H, int Lq, int Lk, int d, int causal,
+                          float scale, const fabft_fault* f,
+                          float* pred, float* actual);
+
+/* Human-readable text for a status code (static storage). */
+const char* fabft_status_str(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FABFT_H */

@@ -1,0 +1,217 @@
+"""Flash-ABFT attention forward on AMD MI355X (gfx950).
+
+Thin Python binding over the C ABI of ``libfabft.so`` (declared in
+``include/fabft.h``): argument marshalling only. Every step of the attention
+and of the checksum runs in the library's HIP kernels; torch supplies device
+memory and the current stream. There is no fallback: if the library is not
+built, every call raises.
+
+    o, resid, flags = attn_fwd(q, k, v, causal=True)       # checksum on
+    o = attn_fwd(q, k, v, causal=True, check=False)         # checksum off
+
+q: [B, H, Lq, d], k and v: [B, H, Lk, d], torch.bfloat16 on the GPU,
+contiguous; d in {64, 128}. scale defaults to 1/sqrt(d).
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from dataclasses import dataclass
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfabft.so")
+
+_vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
+_fp = ctypes.POINTER(ctypes.c_float)
+
+FABFT_OK = 0
+E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD = \
+    -1, -2, -3, -4, -5, -6, -7, -8
+FLAG_RESID, FLAG_NONFINITE = 1, 2
+SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V = 0, 1, 2, 3, 4
+SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V}
+
+
+class FabftFault(ctypes.Structure):
+    _fields_ = [("site", _i), ("b", _i), ("h", _i), ("row", _i), ("col", _i),
+                ("tile", _i), ("bit", _i)]
+
+
+_LIB = None
+
+
+def _load() -> ctypes.CDLL:
+    """Load libfabft.so once; raise if it is not built (no CPU fallback)."""
+    global _LIB
+    if _LIB is not None:
+        return _LIB
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is not built; run `python -m paper_2507_16676_amd.build` "
+            "(hipcc, gfx950). There is no CPU fallback.")
+    L = ctypes.CDLL(LIB_PATH)
+    L.fabft_attn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f]
+    L.fabft_attn_fwd.restype = _i
+    L.fabft_attn_fwd_nocheck.argtypes = [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f]
+    L.fabft_attn_fwd_nocheck.restype = _i
+    L.fabft_attn_fwd_inject.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                        _f, ctypes.POINTER(FabftFault), _vp, _vp]
+    L.fabft_attn_fwd_inject.restype = _i
+    L.fabft_set_stream.argtypes = [_vp]
+    L.fabft_set_stream.restype = None
+    L.fabft_set_threshold.argtypes = [_f, _f]
+    L.fabft_set_threshold.restype = _i
+    L.fabft_get_threshold.argtypes = [_fp, _fp]
+    L.fabft_get_threshold.restype = None
+    L.fabft_key_tile.argtypes = [_i]
+    L.fabft_key_tile.restype = _i
+    L.fabft_query_tile.argtypes = []
+    L.fabft_query_tile.restype = _i
+    L.fabft_status_str.argtypes = [_i]
+    L.fabft_status_str.restype = ctypes.c_char_p
+    _LIB = L
+    return L
+
+
+EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
+           "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
+           "fabft_key_tile", "fabft_query_tile", "fabft_status_str")
+
+
+class FabftError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} (status {status})")
+
+
+def status_str(status: int) -> str:
+    return _load().fabft_status_str(int(status)).decode()
+
+
+def lib() -> ctypes.CDLL:
+    """The loaded C library (for tests of the raw ABI)."""
+    return _load()
+
+
+def _check(rc: int, where: str):
+    if rc != FABFT_OK:
+        raise FabftError(rc, where)
+
+
+def set_threshold(tau_rel: float, tau_abs: float = 0.0):
+    _check(_load().fabft_set_threshold(float(tau_rel), float(tau_abs)), "fabft_set_threshold")
+
+
+def get_threshold() -> tuple[float, float]:
+    a, b = ctypes.c_float(), ctypes.c_float()
+    _load().fabft_get_threshold(ctypes.byref(a), ctypes.byref(b))
+    return a.value, b.value
+
+
+def key_tile(d: int) -> int:
+    r = _load().fabft_key_tile(int(d))
+    _check(min(r, 0), "fabft_key_tile")
+    return r
+
+
+def query_tile() -> int:
+    return _load().fabft_query_tile()
+
+
+def _shape(q, k, v):
+    import torch
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dtype != torch.bfloat16:
+            raise TypeError(f"{name} must be torch.bfloat16, got {t.dtype}")
+        if not t.is_cuda:
+            raise ValueError(f"{name} must be on the GPU")
+        if t.dim() != 4 or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous [B, H, L, d] tensor")
+    B, H, Lq, d = q.shape
+    if tuple(k.shape[:2]) != (B, H) or k.shape[3] != d or tuple(v.shape) != tuple(k.shape):
+        raise ValueError(f"shape mismatch: q {tuple(q.shape)} k {tuple(k.shape)} v {tuple(v.shape)}")
+    return B, H, Lq, k.shape[2], d
+
+
+def _stream(dev):
+    import torch
+    _load().fabft_set_stream(ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
+
+
+def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, check: bool = True,
+             out=None):
+    """Flash-ABFT forward. Returns (o, resid, flags) with check=True, else o.
+
+    out: optional preallocated (o[, resid, flags]) tensors to write into.
+    """
+    import torch
+    B, H, Lq, Lk, d = _shape(q, k, v)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dev = q.device
+    if out is not None:
+        o = out[0]
+    else:
+        o = torch.empty_like(q)
+    _stream(dev)
+    if not check:
+        _check(_load().fabft_attn_fwd_nocheck(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                           B, H, Lq, Lk, d, int(bool(causal)), scale),
+               "fabft_attn_fwd_nocheck")
+        return o
+    if out is not None and len(out) == 3:
+        resid, flags = out[1], out[2]
+    else:
+        resid = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+        flags = torch.empty((B, H, Lq), dtype=torch.uint8, device=dev)
+    _check(_load().fabft_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                               resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
+                               int(bool(causal)), scale), "fabft_attn_fwd")
+    return o, resid, flags
+
+
+@dataclass
+class Fault:
+    """One single-bit fault for attn_fwd_inject (fields as in fabft_fault)."""
+    site: str          # "S", "P", "O", "V" or "none"
+    b: int = 0
+    h: int = 0
+    row: int = 0
+    col: int = 0
+    tile: int = 0
+    bit: int = 0
+
+    def to_c(self) -> FabftFault:
+        return FabftFault(SITES[self.site], self.b, self.h, self.row, self.col, self.tile,
+                          self.bit)
+
+
+def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
+                    fault: Fault | None = None, out=None):
+    """Debug / fault-injection forward. Returns (o, resid, flags, pred, actual)."""
+    import torch
+    B, H, Lq, Lk, d = _shape(q, k, v)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dev = q.device
+    if out is None:
+        o = torch.empty_like(q)
+        resid = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+        flags = torch.empty((B, H, Lq), dtype=torch.uint8, device=dev)
+        pred = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+        actual = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+    else:
+        o, resid, flags, pred, actual = out
+    f = fault.to_c() if fault is not None else None
+    _stream(dev)
+    _check(_load().fabft_attn_fwd_inject(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                      resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
+                                      int(bool(causal)), scale,
+                                      ctypes.byref(f) if f is not None else None,
+                                      pred.data_ptr(), actual.data_ptr()),
+           "fabft_attn_fwd_inject")
+    return o, resid, flags, pred, actual
+
+
+__all__ = ["attn_fwd", "attn_fwd_inject", "Fault", "FabftError", "set_threshold",
+           "get_threshold", "key_tile", "query_tile", "status_str", "lib", "LIB_PATH",
+           "EXPORTS", "FLAG_RESID", "FLAG_NONFINITE"]

@@ -1,0 +1,177 @@
+// C ABI of libfabft.so: argument validation, process-global state (stream,
+// detection threshold) and dispatch to the gfx950 kernels. Every check runs
+// before any launch, so an error status means nothing was written.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <climits>
+#include <cmath>
+#include <cstdint>
+
+#include "../../include/fabft.h"
+#include "fabft_kernels.h"
+
+namespace {
+
+hipStream_t g_stream = nullptr;
+// Default relative threshold; a row is flagged when |r| > tau_rel * M + tau_abs
+// with M = sum_j |O_ij| + |pred_i|.
+float g_tau_rel = 1.0f / 4096.0f;
+float g_tau_abs = 0.0f;
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int validate(const void* q, const void* k, const void* v, void* o, int B, int H, int Lq,
+             int Lk, int d, float scale, int* n_qt, int* grid) {
+  if (!q || !k || !v || !o) return FABFT_E_NULL;
+  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  if (B < 1 || H < 1 || Lq < 1 || Lk < 1) return FABFT_E_SHAPE;
+  if (!std::isfinite(scale) || scale < 0.f) return FABFT_E_SCALE;
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return FABFT_E_ALIGN;
+  const long long nqt = (static_cast<long long>(Lq) + fabft::kQueryTile - 1) / fabft::kQueryTile;
+  const long long g = static_cast<long long>(B) * H * nqt;
+  // grid index and per-row index arithmetic in the kernel is 32-bit
+  if (g > INT_MAX || static_cast<long long>(B) * H > INT_MAX / 2) return FABFT_E_SHAPE;
+  *n_qt = static_cast<int>(nqt);
+  *grid = static_cast<int>(g);
+  return FABFT_OK;
+}
+
+fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* o,
+                             float* resid, uint8_t* flags, int Lq, int Lk, float scale,
+                             int n_qt, int grid) {
+  fabft::FwdParams p{};
+  p.q = static_cast<const uint16_t*>(q);
+  p.k = static_cast<const uint16_t*>(k);
+  p.v = static_cast<const uint16_t*>(v);
+  p.o = static_cast<uint16_t*>(o);
+  p.resid = resid;
+  p.flags = flags;
+  p.pred = nullptr;
+  p.actual = nullptr;
+  p.Lq = Lq;
+  p.Lk = Lk;
+  p.n_qt = n_qt;
+  p.grid = grid;
+  p.sl2 = scale * kLog2e;
+  p.tau_rel = g_tau_rel;
+  p.tau_abs = g_tau_abs;
+  p.f_site = 0;
+  p.f_bh = p.f_row = p.f_col = p.f_tile = p.f_bit = -1;
+  return p;
+}
+
+int launch(const fabft::FwdParams& p, int d, int causal, int mode) {
+  const int rc = fabft::launch_fwd(p, d, causal != 0, mode, g_stream);
+  return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
+}
+
+}  // namespace
+
+extern "C" {
+
+int fabft_attn_fwd(const void* q, const void* k, const void* v, void* o, float* resid,
+                   uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                   float scale) {
+  int n_qt = 0, grid = 0;
+  int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
+  if (rc != FABFT_OK) return rc;
+  if (!resid || !flags) return FABFT_E_NULL;
+  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid), d, causal, 1);
+}
+
+int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o, int B, int H,
+                           int Lq, int Lk, int d, int causal, float scale) {
+  int n_qt = 0, grid = 0;
+  int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
+  if (rc != FABFT_OK) return rc;
+  return launch(make_params(q, k, v, o, nullptr, nullptr, Lq, Lk, scale, n_qt, grid), d,
+                causal, 0);
+}
+
+int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,
+                          uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                          float scale, const fabft_fault* f, float* pred, float* actual) {
+  int n_qt = 0, grid = 0;
+  int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
+  if (rc != FABFT_OK) return rc;
+  if (!resid || !flags) return FABFT_E_NULL;
+  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid);
+  p.pred = pred;
+  p.actual = actual;
+  if (f && f->site != FABFT_SITE_NONE) {
+    if (f->b < 0 || f->b >= B || f->h < 0 || f->h >= H) return FABFT_E_FAULT;
+    const int off = Lk - Lq;
+    const int bc = fabft::key_tile(d);
+    switch (f->site) {
+      case FABFT_SITE_S:
+      case FABFT_SITE_P:
+        if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= Lk) return FABFT_E_FAULT;
+        if (causal && f->col > f->row + off) return FABFT_E_FAULT;
+        if (f->bit < 0 || f->bit >= (f->site == FABFT_SITE_S ? 32 : 16)) return FABFT_E_FAULT;
+        break;
+      case FABFT_SITE_O: {
+        if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= d) return FABFT_E_FAULT;
+        if (f->bit < 0 || f->bit >= 32) return FABFT_E_FAULT;
+        const long long last = causal ? std::min<long long>(Lk - 1, (long long)f->row + off)
+                                      : (long long)Lk - 1;
+        if (last < 0 || f->tile < 0 || (long long)f->tile * bc > last) return FABFT_E_FAULT;
+        break;
+      }
+      case FABFT_SITE_V:
+        if (f->row < 0 || f->row >= Lk || f->col < 0 || f->col >= d) return FABFT_E_FAULT;
+        if (f->tile < 0 || f->tile >= n_qt) return FABFT_E_FAULT;
+        if (f->bit < 0 || f->bit >= 16) return FABFT_E_FAULT;
+        break;
+      default:
+        return FABFT_E_FAULT;
+    }
+    p.f_site = f->site;
+    p.f_bh = f->b * H + f->h;
+    p.f_row = f->row;
+    p.f_col = f->col;
+    p.f_tile = f->tile;
+    p.f_bit = f->bit;
+  }
+  return launch(p, d, causal, 2);
+}
+
+void fabft_set_stream(void* hip_stream) { g_stream = static_cast<hipStream_t>(hip_stream); }
+
+int fabft_set_threshold(float tau_rel, float tau_abs) {
+  if (!(tau_rel >= 0.f) || !(tau_abs >= 0.f)) return FABFT_E_THRESHOLD;
+  g_tau_rel = tau_rel;
+  g_tau_abs = tau_abs;
+  return FABFT_OK;
+}
+
+void fabft_get_threshold(float* tau_rel, float* tau_abs) {
+  if (tau_rel) *tau_rel = g_tau_rel;
+  if (tau_abs) *tau_abs = g_tau_abs;
+}
+
+int fabft_key_tile(int d) {
+  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  return fabft::key_tile(d);
+}
+
+int fabft_query_tile(void) { return fabft::kQueryTile; }
+
+const char* fabft_status_str(int status) {
+  switch (status) {
+    case FABFT_OK: return "ok";
+    case FABFT_E_NULL: return "null pointer argument";
+    case FABFT_E_SHAPE: return "invalid shape (B, H, Lq, Lk must be >= 1; grid too large)";
+    case FABFT_E_HEADDIM: return "unsupported head dimension (d must be 64 or 128)";
+    case FABFT_E_ALIGN: return "q, k, v and o must be 16-byte aligned";
+    case FABFT_E_LAUNCH: return "kernel launch failed";
+    case FABFT_E_SCALE: return "scale must be finite and >= 0";
+    case FABFT_E_FAULT: return "fault descriptor out of range";
+    case FABFT_E_THRESHOLD: return "threshold must be >= 0";
+    default: return "unknown status";
+  }
+}
+
+}  // extern "C"

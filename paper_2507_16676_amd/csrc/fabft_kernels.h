@@ -1,0 +1,35 @@
+// Internal interface between the C-ABI host code and the gfx950 kernels.
+#ifndef FABFT_KERNELS_H
+#define FABFT_KERNELS_H
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace fabft {
+
+constexpr int kQueryTile = 128;  // query rows per workgroup
+
+struct FwdParams {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  uint16_t* o;
+  float* resid;
+  uint8_t* flags;
+  float* pred;    // injection/debug kernels only; may be null
+  float* actual;  // injection/debug kernels only; may be null
+  int Lq, Lk;
+  int n_qt;       // query tiles per head
+  int grid;       // workgroups = B * H * n_qt
+  float sl2;      // scale * log2(e)
+  float tau_rel, tau_abs;
+  int f_site, f_bh, f_row, f_col, f_tile, f_bit;  // fault (site 0 = none)
+};
+
+// mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection
+int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream);
+int key_tile(int d);
+
+}  // namespace fabft
+
+#endif

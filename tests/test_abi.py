@@ -1,0 +1,115 @@
+"""Host-side tests of the C ABI: the library loads, exports every symbol the
+header declares, and rejects bad arguments before launching anything (these
+calls never reach a kernel, so they run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2507_16676_amd as F
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fabft.h")
+
+# fake, 16-byte aligned, never dereferenced: validation fails before a launch
+P = 4096
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fabft_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = _declared()
+    assert "fabft_attn_fwd" in names and "fabft_attn_fwd_nocheck" in names
+    lib = F.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(F.EXPORTS) == set(names)
+
+
+def test_status_strings():
+    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8):
+        assert F.status_str(s) and F.status_str(s) != "unknown status"
+    assert F.status_str(12345) == "unknown status"
+
+
+def test_key_and_query_tiles():
+    assert F.key_tile(128) == 64
+    assert F.key_tile(64) == 64
+    assert F.query_tile() == 128
+    with pytest.raises(F.FabftError):
+        F.key_tile(96)
+
+
+def test_threshold_validation_and_roundtrip():
+    old = F.get_threshold()
+    try:
+        F.set_threshold(1e-3, 2e-6)
+        assert F.get_threshold() == pytest.approx((1e-3, 2e-6))
+        lib = F.lib()
+        assert lib.fabft_set_threshold(-1.0, 0.0) == F.E_THRESHOLD
+        assert lib.fabft_set_threshold(float("nan"), 0.0) == F.E_THRESHOLD
+        assert lib.fabft_set_threshold(0.0, -1.0) == F.E_THRESHOLD
+        assert F.get_threshold() == pytest.approx((1e-3, 2e-6))
+    finally:
+        F.set_threshold(*old)
+
+
+@pytest.mark.parametrize("args,code", [
+    ((0, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
+    ((P, P, P, P, 0, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
+    ((P, P, P, P, P, 0, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 96, 0, 1.0), F.E_HEADDIM),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 256, 0, 1.0), F.E_HEADDIM),
+    ((P, P, P, P, P, P, 0, 1, 8, 8, 128, 0, 1.0), F.E_SHAPE),
+    ((P, P, P, P, P, P, 1, 0, 8, 8, 128, 0, 1.0), F.E_SHAPE),
+    ((P, P, P, P, P, P, 1, 1, 0, 8, 128, 0, 1.0), F.E_SHAPE),
+    ((P, P, P, P, P, P, 1, 1, 8, -3, 128, 0, 1.0), F.E_SHAPE),
+    ((P, P, P, P, P, P, 65536, 65536, 1024, 8, 128, 0, 1.0), F.E_SHAPE),
+    ((P + 2, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_ALIGN),
+    ((P, P, P + 8, P, P, P, 1, 1, 8, 8, 64, 0, 1.0), F.E_ALIGN),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, -0.5), F.E_SCALE),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, float("nan")), F.E_SCALE),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 128, 1, float("inf")), F.E_SCALE),
+])
+def test_fwd_rejects_bad_arguments(args, code):
+    assert F.lib().fabft_attn_fwd(*args) == code
+
+
+def test_nocheck_rejects_bad_arguments():
+    lib = F.lib()
+    assert lib.fabft_attn_fwd_nocheck(P, P, P, 0, 1, 1, 8, 8, 128, 0, 1.0) == F.E_NULL
+    assert lib.fabft_attn_fwd_nocheck(P, P, P, P, 1, 1, 8, 8, 32, 0, 1.0) == F.E_HEADDIM
+    assert lib.fabft_attn_fwd_nocheck(P, P, P, P, 1, 1, 8, 8, 64, 0, -1.0) == F.E_SCALE
+
+
+@pytest.mark.parametrize("fault", [
+    F.Fault("S", b=1, row=0, col=0),              # b out of range (B=1)
+    F.Fault("S", h=2, row=0, col=0),              # h out of range (H=2)
+    F.Fault("S", row=8, col=0),                   # row >= Lq
+    F.Fault("S", row=3, col=5),                   # causal: key 5 not visible to query 3
+    F.Fault("S", row=3, col=0, bit=32),
+    F.Fault("P", row=3, col=0, bit=16),
+    F.Fault("O", row=3, col=128, tile=0),         # col >= d
+    F.Fault("O", row=3, col=0, tile=1),           # tile beyond the row's keys
+    F.Fault("O", row=3, col=0, tile=-1),
+    F.Fault("V", row=8, col=0, tile=0),           # key >= Lk
+    F.Fault("V", row=0, col=0, tile=1),           # only one query tile
+    F.Fault("V", row=0, col=0, tile=0, bit=16),
+])
+def test_inject_rejects_bad_faults(fault):
+    f = fault.to_c()
+    rc = F.lib().fabft_attn_fwd_inject(P, P, P, P, P, P, 1, 2, 8, 8, 128, 1, 0.1,
+                                       ctypes.byref(f), None, None)
+    assert rc == F.E_FAULT
+
+
+def test_inject_rejects_unknown_site():
+    f = F.FabftFault(9, 0, 0, 0, 0, 0, 0)
+    rc = F.lib().fabft_attn_fwd_inject(P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 0.1,
+                                       ctypes.byref(f), None, None)
+    assert rc == F.E_FAULT

@@ -1,0 +1,103 @@
+"""Fault-injection path on the GPU: single bit flips at the S, P, O and V
+sites change O only where they should, and the per-row check flags the rows
+whose output moved by more than the threshold (P, O, V); S-site flips before
+the checksum tap change O and pred consistently."""
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from tests import gpu_helpers as G
+
+pytestmark = pytest.mark.gpu
+
+F = pytest.importorskip("paper_2507_16676_amd")
+
+W_INJ = W.Workload("inject", 1, 2, 300, 300, 128, True, 128 ** -0.5, seed=7)
+
+
+@pytest.fixture(scope="module")
+def golden():
+    inp = W.make_inputs(W_INJ)
+    q, k, v = G.dev_inputs(inp)
+    out = F.attn_fwd_inject(q, k, v, causal=True, scale=W_INJ.scale)
+    torch.cuda.synchronize()
+    assert int(out[2].sum()) == 0
+    return (q, k, v), out
+
+
+def _inject(golden, fault):
+    (q, k, v), _ = golden
+    print(f"[inject] {fault}", flush=True)
+    out = F.attn_fwd_inject(q, k, v, causal=True, scale=W_INJ.scale, fault=fault)
+    torch.cuda.synchronize()
+    return out
+
+
+def _changed_rows(a, b):
+    d = (a.view(torch.int16) != b.view(torch.int16)).any(dim=-1)
+    return set(map(tuple, d.nonzero().cpu().numpy().tolist()))
+
+
+def test_no_fault_matches_production(golden):
+    (q, k, v), (o, resid, flags, pred, actual) = golden
+    o2, r2, f2 = F.attn_fwd(q, k, v, causal=True, scale=W_INJ.scale)
+    torch.cuda.synchronize()
+    assert torch.equal(o.view(torch.int16), o2.view(torch.int16))
+    assert torch.equal(resid.view(torch.int32), r2.view(torch.int32))
+    # resid is exactly pred - actual
+    assert torch.equal(resid, pred - actual)
+
+
+@pytest.mark.parametrize("bit", [30, 27, 23])
+def test_o_site_flip(golden, bit):
+    f = F.Fault("O", b=0, h=1, row=200, col=37, tile=2, bit=bit)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    (_, (o0, r0, f0, p0, a0)) = golden
+    changed = _changed_rows(o, o0)
+    assert changed <= {(0, 1, 200)}
+    # pred does not see an output-accumulator fault
+    assert torch.equal(pred, p0)
+    others = flags.clone()
+    others[0, 1, 200] = 0
+    assert int(others.sum()) == 0
+    if bit == 30:
+        # the top exponent bit moves o_ij by a factor 2^128 (or from 0 to 2)
+        assert changed == {(0, 1, 200)}
+        assert int(flags[0, 1, 200]) != 0
+
+
+def test_p_site_flip(golden):
+    f = F.Fault("P", b=0, h=0, row=250, col=100, bit=14)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    (_, (o0, r0, f0, p0, a0)) = golden
+    assert _changed_rows(o, o0) == {(0, 0, 250)}
+    assert int(flags[0, 0, 250]) != 0
+    assert int(flags.sum()) == int(flags[0, 0, 250])
+
+
+def test_v_site_flip(golden):
+    # key 100, column 5, in the workgroup holding query rows 128..255
+    f = F.Fault("V", b=0, h=1, row=100, col=5, tile=1, bit=14)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    (_, (o0, r0, f0, p0, a0)) = golden
+    changed = _changed_rows(o, o0)
+    assert changed and all(h == 1 and 128 <= i < 256 for _, h, i in changed)
+    flagged = set(map(tuple, (flags != 0).nonzero().cpu().numpy().tolist()))
+    assert flagged and flagged <= {(0, 1, i) for i in range(128, 256)}
+    # every row whose output moved by more than 2^-8 of its max is flagged
+    O = G.from_dev_bf16(o)[0, 1]
+    O0 = G.from_dev_bf16(o0)[0, 1]
+    big = np.where(np.abs(O - O0).max(axis=1) > 2 ** -8 * np.abs(O0).max(axis=1))[0]
+    assert set((0, 1, int(i)) for i in big) <= flagged
+
+
+def test_s_site_flip_is_consistent(golden):
+    # a score flip before the checksum tap moves O and pred together
+    f = F.Fault("S", b=0, h=0, row=120, col=3, bit=26)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    (_, (o0, r0, f0, p0, a0)) = golden
+    assert _changed_rows(o, o0) <= {(0, 0, 120)}
+    others = flags.clone()
+    others[0, 0, 120] = 0
+    assert int(others.sum()) == 0
