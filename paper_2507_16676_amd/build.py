@@ -28,27 +28,49 @@ def hipcc_path() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libfabft.so)")
 
 
-def build_cmd(out: str, extra=()) -> list[str]:
-    return [hipcc_path(), f"--offload-arch={ARCH}", "-O3", "-std=c++17",
-            "-shared", "-fPIC", "-x", "hip",
-            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-            "-I", os.path.join(ROOT, "include"), *extra, "-o", out, *SOURCES]
+COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+# Kernels only: IEEE mode off, so max/min need no NaN-quieting of their inputs
+# (needs relaxed NaN rules; the kernels test non-finite values on the bits and
+# a NaN score still reaches exp2 and propagates into o, l and c).
+KERNEL_FLAGS = ["-mno-amdgpu-ieee", "-fno-honor-nans"]
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    tmp = LIB + f".tmp{os.getpid()}"
-    cmd = build_cmd(tmp, extra)
+def build_cmds(out: str, objdir: str, extra=()) -> list[list[str]]:
+    inc = ["-I", os.path.join(ROOT, "include")]
+    hipcc = hipcc_path()
+    k_obj = os.path.join(objdir, "fabft_kernels.o")
+    a_obj = os.path.join(objdir, "fabft_api.o")
+    return [
+        [hipcc, "-x", "hip", *COMMON, *KERNEL_FLAGS, *inc, *extra, "-c", SOURCES[0], "-o", k_obj],
+        [hipcc, "-x", "hip", *COMMON, *inc, *extra, "-c", SOURCES[1], "-o", a_obj],
+        [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", k_obj, a_obj, "-o", out],
+    ]
+
+
+def _run(cmd, verbose):
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     msgs = "\n".join(line for line in (res.stdout + res.stderr).splitlines()
                      if "packed-fp32-ops" not in line)
     if res.returncode != 0:
-        if os.path.exists(tmp):
-            os.unlink(tmp)
-        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{msgs}")
+        raise RuntimeError(f"hipcc failed ({res.returncode}):\n{' '.join(cmd)}\n{msgs}")
     if verbose and msgs.strip():
         print(msgs, flush=True)
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    import tempfile
+    tmp = LIB + f".tmp{os.getpid()}"
+    with tempfile.TemporaryDirectory(prefix="fabft_build_") as objdir:
+        try:
+            for cmd in build_cmds(tmp, objdir, extra):
+                _run(cmd, verbose)
+        except Exception:
+            if os.path.exists(tmp):
+                os.unlink(tmp)
+            raise
     os.replace(tmp, LIB)
     return LIB
 
