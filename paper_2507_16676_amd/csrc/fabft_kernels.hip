@@ -107,6 +107,11 @@ __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
+// V^T row r keeps its 8-key (16-byte) chunks in the order c ^ ((r >> 4) & 7):
+// the loader's 8-byte writes (16 lanes on rows 8 apart) and the MFMA operand
+// reads (16 lanes on consecutive rows) then fall in distinct LDS banks.
+__device__ __forceinline__ int vt_chunk(int row, int c) { return c ^ ((row >> 4) & 7); }
+
 // One LDS stage: a K tile, its V^T and sumrow(V) as bf16 hi/lo key pairs.
 template <int D>
 struct Stage {
@@ -268,7 +273,8 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdParams p) {
       for (int r = 0; r < KPT / 2; ++r)
         w[r] = (j & 1) == 0 ? (vreg[2 * r][e] & 0xffffu) | (vreg[2 * r + 1][e] << 16)
                             : (vreg[2 * r][e] >> 16) | (vreg[2 * r + 1][e] & 0xffff0000u);
-      uint16_t* dst = &st.vt[(8 * lc + j) * VST + KPT * lkg];
+      const int row = 8 * lc + j, key = KPT * lkg;
+      uint16_t* dst = &st.vt[row * VST + 8 * vt_chunk(row, key >> 3) + (key & 7)];
       if constexpr (KPT == 4)
         *reinterpret_cast<u32x2*>(dst) = u32x2{w[0], w[1]};
       else
@@ -436,8 +442,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdParams p) {
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
+          const int row = 32 * db + mrow;
           const u32x4 a = *reinterpret_cast<const u32x4*>(
-              &st.vt[(32 * db + mrow) * VST + 32 * kb + 16 * h + 8 * grp]);
+              &st.vt[row * VST + 8 * vt_chunk(row, 4 * kb + 2 * h + grp)]);
           oacc[db] = mfma32(a, pb[kb][h], oacc[db]);
         }
     if constexpr (INJECT) {
