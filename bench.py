@@ -115,8 +115,8 @@ def cpu_baseline(w, target_s: float):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="dec_l4096")
     ap.add_argument("--rounds", type=int, default=5,
                     help="interleaved on/off rounds for the overhead figure")

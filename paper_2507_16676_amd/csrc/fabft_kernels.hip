@@ -92,8 +92,24 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
-// value held by lane (i ^ 32)
-__device__ __forceinline__ float xor32(float x) { return __shfl_xor(x, 32); }
+// Combine the values of lanes i and i ^ 32 with a symmetric operation:
+// v_permlane32_swap leaves (own, partner) in the two results of every lane.
+__device__ __forceinline__ float sum_xor32(float x) {
+#ifdef FABFT_SHFL_XOR32
+  return x + __shfl_xor(x, 32);
+#else
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+#endif
+}
+__device__ __forceinline__ float max_xor32(float x) {
+#ifdef FABFT_SHFL_XOR32
+  return __builtin_fmaxf(x, __shfl_xor(x, 32));
+#else
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+#endif
+}
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   f32x2 f = {a, b};
@@ -125,7 +141,10 @@ struct Stage {
 };
 
 template <int D, bool CAUSAL, bool CHECK, bool INJECT>
-__global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdParams p) {
+#ifndef FABFT_MIN_BLOCKS
+#define FABFT_MIN_BLOCKS 2
+#endif
+__global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdParams p) {
   constexpr int BC = TileCfg<D>::BC;
   constexpr int KPT = TileCfg<D>::KPT;
   constexpr int KST = Stage<D>::KST;
@@ -351,7 +370,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int i = 0; i < 16; i += 2)
         mx = __builtin_fmaxf(mx, __builtin_fmaxf(sacc[kb][i], sacc[kb][i + 1]));
-    mx = __builtin_fmaxf(mx, xor32(mx));
+    mx = max_xor32(mx);
     // lazy running max in the exp2 domain
     const float mt2 = (mx == -__builtin_inff()) ? -__builtin_inff() : mx * sl2;
     const float m2_new = (mt2 > m2_run + kLazy) ? mt2 : m2_run;
@@ -436,12 +455,13 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
     }
+    // (output blocks innermost: consecutive MFMAs accumulate independently)
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+    for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
+      for (int h = 0; h < 2; ++h)
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
+        for (int db = 0; db < NDB; ++db) {
           const int row = 32 * db + mrow;
           const u32x4 a = *reinterpret_cast<const u32x4*>(
               &st.vt[row * VST + 8 * vt_chunk(row, 4 * kb + 2 * h + grp)]);
@@ -466,7 +486,7 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdParams p) {
   }
 
   // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
-  const float l_tot = l_run + xor32(l_run);
+  const float l_tot = sum_xor32(l_run);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   float act = 0.f, absum = 0.f;
 #pragma unroll
@@ -490,9 +510,9 @@ __global__ __launch_bounds__(kThreads, 2) void fwd_kernel(FwdParams p) {
       }
   }
   if constexpr (CHECK) {
-    act += xor32(act);
-    absum += xor32(absum);
-    const float c_tot = c_run + xor32(c_run);
+    act = sum_xor32(act);
+    absum = sum_xor32(absum);
+    const float c_tot = sum_xor32(c_run);
     const float pred = c_tot * inv;
     const float r = pred - act;
     const float M = absum + __builtin_fabsf(pred);
