@@ -87,7 +87,7 @@ void fabft_set_stream(void* hip_stream);
 
 /*
  * Detection threshold: a row is flagged when NOT |r| <= tau_rel*M + tau_abs
- * (so a NaN residual is flagged). Defaults: tau_rel = 2^-12, tau_abs = 0.
+ * (so a NaN residual is flagged). Defaults: tau_rel = 2^-16, tau_abs = 0.
  * Returns FABFT_E_THRESHOLD (and keeps the old values) for negative or NaN.
  */
 int fabft_set_threshold(float tau_rel, float tau_abs);

@@ -1,0 +1,299 @@
+"""Fault-injection campaign and fault-free sweep for the Flash-ABFT kernel.
+
+Section IV-B of the paper flips one bit per run at a random time in a random
+register and sorts each run into Detected / False positive / Silent. Here a
+run flips one bit at one of the kernel's fault sites (S, P, O, V; see
+include/fabft.h), chosen uniformly, at a uniformly drawn live element and
+bit, and compares the faulty output with the fault-free output of the same
+kernel (which is bitwise deterministic):
+
+  significant   some |O_ij - O*_ij| > 2^-8 * max_j |O*_ij| in a row, or a
+                non-finite O_ij (O* = fault-free output of that row)
+  flagged       some row of the head has a nonzero flag
+
+  Detected = flagged and significant; Detected (minor) = flagged, output
+  changed but not significantly; False positive = flagged while the output
+  is bitwise unchanged (an alarm with a correct result, the paper's sense);
+  Silent = not flagged and significant; Benign = none of these.
+
+The headline rate is Detected / (Detected + Silent) over exponent-bit flips
+(fp32 bits 23-30, bf16 bits 7-14) at the P, O and V sites; S-site flips
+happen before the checksum tap and change O and pred consistently, so they
+are reported separately.
+
+Only the faulted head is recomputed per run (heads are independent, and the
+per-head computation does not depend on the others). Runs are drawn from
+numpy PCG64(run id), so a campaign is reproducible and resumable.
+
+    python -m paper_2507_16676_amd.campaign campaign --runs 10000 --out c.jsonl
+    python -m paper_2507_16676_amd.campaign sweep --seeds 10000 --out s.json
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+SITES = ("S", "P", "O", "V")
+SITE_BITS = {"S": 32, "P": 16, "O": 32, "V": 16}
+EXP_BITS = {"S": range(23, 31), "P": range(7, 15), "O": range(23, 31), "V": range(7, 15)}
+SIG_REL = 2.0 ** -8
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def device_inputs(w, seed, device="cuda"):
+    """Seeded N(0,1) bf16 inputs of workload w drawn on the GPU (same
+    recipe as the benchmark)."""
+    torch = _torch()
+    g = torch.Generator(device=device)
+    g.manual_seed(int(seed))
+    q = torch.randn((w.B, w.H, w.Lq, w.d), generator=g, device=device)
+    k = torch.randn((w.B, w.H, w.Lk, w.d), generator=g, device=device)
+    v = torch.randn((w.B, w.H, w.Lk, w.d), generator=g, device=device)
+    if w.qk_prescale != 1.0:
+        q *= w.qk_prescale
+        k *= w.qk_prescale
+    if w.peaked_frac > 0:
+        n = int(round(w.peaked_frac * w.Lk))
+        gc = torch.Generator()
+        gc.manual_seed(int(seed) + 1)
+        for b in range(w.B):
+            for h in range(w.H):
+                idx = torch.randperm(w.Lk, generator=gc)[:n].to(device)
+                k[b, h, idx] *= w.peaked_mult
+    return (q.to(torch.bfloat16).contiguous(), k.to(torch.bfloat16).contiguous(),
+            v.to(torch.bfloat16).contiguous())
+
+
+def draw_fault(run: int, w, key_tile: int, query_tile: int, sites=SITES):
+    """The fault of run `run`: site, head, element and bit, uniform over live
+    elements (visible keys for S/P, processed key tiles for O, query tiles
+    that can see the key for V)."""
+    from . import Fault
+    rng = np.random.default_rng(int(run))
+    site = sites[int(rng.integers(len(sites)))]
+    b = int(rng.integers(w.B))
+    h = int(rng.integers(w.H))
+    off = w.Lk - w.Lq
+    bit = int(rng.integers(SITE_BITS[site]))
+    if site in ("S", "P", "O"):
+        while True:
+            row = int(rng.integers(w.Lq))
+            last = min(w.Lk - 1, row + off) if w.causal else w.Lk - 1
+            if last >= 0:
+                break
+        if site == "O":
+            col = int(rng.integers(w.d))
+            tile = int(rng.integers(last // key_tile + 1))
+        else:
+            col = int(rng.integers(last + 1))
+            tile = 0
+        return Fault(site, b, h, row, col, tile, bit)
+    # V: key k, column j, one query tile whose rows can see key k
+    n_qt = (w.Lq + query_tile - 1) // query_tile
+    while True:
+        key = int(rng.integers(w.Lk))
+        first = 0
+        if w.causal:
+            lo_row = key - off          # first row that sees the key
+            if lo_row >= w.Lq:
+                continue
+            first = max(0, lo_row) // query_tile
+        break
+    col = int(rng.integers(w.d))
+    tile = int(rng.integers(first, n_qt))
+    return Fault("V", b, h, key, col, tile, bit)
+
+
+def classify(o, o_gold, flags):
+    """Outcome of one run on one head: tensors [L, d] (bf16) and [L] (u8)."""
+    torch = _torch()
+    of = o.float()
+    og = o_gold.float()
+    diff = (of - og).abs()
+    nonfinite_rows = ~torch.isfinite(of).all(dim=1)
+    ref = og.abs().amax(dim=1)
+    sig_rows = (diff > SIG_REL * ref[:, None]).any(dim=1) | nonfinite_rows
+    flag_rows = flags != 0
+    n_sig = int(sig_rows.sum())
+    n_flag = int(flag_rows.sum())
+    n_sig_unflagged = int((sig_rows & ~flag_rows).sum())
+    changed = int((o.view(torch.int16) != o_gold.view(torch.int16)).any(dim=1).sum())
+    sig, flg = n_sig > 0, n_flag > 0
+    outcome = ("detected" if flg and sig else
+               "detected_minor" if flg and changed else
+               "false_positive" if flg else
+               "silent" if sig else "benign")
+    return {"outcome": outcome, "rows_changed": changed, "rows_significant": n_sig,
+            "rows_flagged": n_flag, "rows_significant_unflagged": n_sig_unflagged,
+            "nonfinite": bool(nonfinite_rows.any())}
+
+
+def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES):
+    """Run faults start..runs-1 on workload w (inputs drawn with `seed`),
+    appending one JSON line per run to out_path; runs already in the file
+    are skipped."""
+    torch = _torch()
+    from . import attn_fwd_inject, key_tile, query_tile
+    done = set()
+    if os.path.exists(out_path):
+        with open(out_path) as f:
+            for line in f:
+                try:
+                    done.add(json.loads(line)["run"])
+                except (ValueError, KeyError):
+                    pass
+    q, k, v = device_inputs(w, seed)
+    bc, qt = key_tile(w.d), query_tile()
+    gold = {}
+    t0 = time.time()
+    n_new = 0
+    with open(out_path, "a") as out:
+        for r in range(start, runs):
+            if r in done:
+                continue
+            f = draw_fault(r, w, bc, qt, sites)
+            b, h = f.b, f.h
+            qh, kh, vh = q[b:b + 1, h:h + 1], k[b:b + 1, h:h + 1], v[b:b + 1, h:h + 1]
+            if (b, h) not in gold:
+                og, _, fg, _, _ = attn_fwd_inject(qh, kh, vh, causal=w.causal, scale=w.scale)
+                torch.cuda.synchronize()
+                assert int(fg.sum()) == 0, f"fault-free head ({b},{h}) flagged"
+                gold[(b, h)] = og
+            f_local = type(f)(f.site, 0, 0, f.row, f.col, f.tile, f.bit)
+            o, resid, flags, pred, actual = attn_fwd_inject(qh, kh, vh, causal=w.causal,
+                                                            scale=w.scale, fault=f_local)
+            res = classify(o[0, 0], gold[(b, h)][0, 0], flags[0, 0])
+            rec = {"run": r, "site": f.site, "b": b, "h": h, "row": f.row, "col": f.col,
+                   "tile": f.tile, "bit": f.bit,
+                   "exponent_bit": f.bit in EXP_BITS[f.site], **res}
+            out.write(json.dumps(rec) + "\n")
+            n_new += 1
+            if log_every and n_new % log_every == 0:
+                out.flush()
+                print(f"[campaign] {n_new} runs, {time.time() - t0:.1f} s", flush=True)
+    return summarize(out_path)
+
+
+def summarize(path):
+    recs = [json.loads(l) for l in open(path) if l.strip()]
+    table = {}
+    for r in recs:
+        for key in (("all", r["site"]), ("bit", r["site"], r["bit"])):
+            t = table.setdefault(key, {"detected": 0, "detected_minor": 0,
+                                       "false_positive": 0, "silent": 0, "benign": 0})
+            t[r["outcome"]] += 1
+
+    def wilson(k, n, z=1.96):
+        if n == 0:
+            return (0.0, 0.0)
+        p = k / n
+        den = 1 + z * z / n
+        c = (p + z * z / (2 * n)) / den
+        hw = z * math.sqrt(p * (1 - p) / n + z * z / (4 * n * n)) / den
+        return (max(0.0, c - hw), min(1.0, c + hw))
+
+    head = {"detected": 0, "silent": 0}
+    for r in recs:
+        if r["site"] in ("P", "O", "V") and r["exponent_bit"]:
+            if r["outcome"] in head:
+                head[r["outcome"]] += 1
+    n = head["detected"] + head["silent"]
+    rate = head["detected"] / n if n else float("nan")
+    per_site = {}
+    for s in SITES:
+        t = table.get(("all", s), {})
+        tot = sum(t.values())
+        per_site[s] = {**t, "runs": tot,
+                       "raw_detect_rate": (t.get("detected", 0) / tot) if tot else None}
+    per_bit = {f"{s}{b}": table[("bit", s, b)] for (_, s, b) in
+               sorted(k for k in table if k[0] == "bit")}
+    return {"runs": len(recs),
+            "headline": {"what": "exponent-bit flips at P, O, V: detected / (detected + silent)",
+                         "detected": head["detected"], "silent": head["silent"],
+                         "rate": rate, "wilson95": wilson(head["detected"], n)},
+            "false_positives": sum(1 for r in recs if r["outcome"] == "false_positive"),
+            "per_site": per_site, "per_bit": per_bit}
+
+
+def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000):
+    """Fault-free runs on seeds seed0..seed0+seeds-1: count flagged rows
+    (must be 0) and track rho = max |resid| / (sum_j |O_ij| + |pred|)."""
+    torch = _torch()
+    from . import attn_fwd, attn_fwd_inject, get_threshold
+    o = resid = flags = None
+    flagged_total = 0
+    flagged_seeds = []
+    rho_max, rho_seeds = 0.0, 0
+    t0 = time.time()
+    for i in range(seeds):
+        s = seed0 + i
+        q, k, v = device_inputs(w, s)
+        o, resid, flags = attn_fwd(q, k, v, causal=w.causal, scale=w.scale)
+        nf = int((flags != 0).sum())
+        if nf:
+            flagged_total += nf
+            flagged_seeds.append(s)
+        if rho_every and i % rho_every == 0:
+            od, rd, fd, pred, actual = attn_fwd_inject(q, k, v, causal=w.causal, scale=w.scale)
+            M = od.float().abs().sum(dim=-1) + pred.abs()
+            ratio = (rd.abs() / M.clamp_min(1e-30)).max().item()
+            rho_max = max(rho_max, ratio)
+            rho_seeds += 1
+        if log_every and (i + 1) % log_every == 0:
+            print(f"[sweep] {i + 1} seeds, flagged rows {flagged_total}, rho max {rho_max:.3e}, "
+                  f"{time.time() - t0:.1f} s", flush=True)
+    rows = seeds * w.B * w.H * w.Lq
+    res = {"workload": w.name, "seeds": seeds, "seed0": seed0, "rows_checked": rows,
+           "flagged_rows": flagged_total, "flagged_seeds": flagged_seeds[:100],
+           "rho_max": rho_max, "rho_seeds": rho_seeds, "threshold": get_threshold(),
+           "seconds": time.time() - t0}
+    if out_path:
+        with open(out_path, "w") as f:
+            json.dump(res, f, indent=1)
+    return res
+
+
+def main(argv=None):
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
+    import workloads as W
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="cmd", required=True)
+    c = sub.add_parser("campaign")
+    c.add_argument("--workload", default="dec_l4096")
+    c.add_argument("--runs", type=int, default=10000)
+    c.add_argument("--start", type=int, default=0)
+    c.add_argument("--seed", type=int, default=0)
+    c.add_argument("--out", required=True)
+    c.add_argument("--summary")
+    s = sub.add_parser("sweep")
+    s.add_argument("--workload", default="dec_l4096")
+    s.add_argument("--seeds", type=int, default=10000)
+    s.add_argument("--seed0", type=int, default=1)
+    s.add_argument("--rho-every", type=int, default=100)
+    s.add_argument("--out", required=True)
+    a = ap.parse_args(argv)
+    w = W.WORKLOADS[a.workload]
+    if a.cmd == "campaign":
+        summ = run_campaign(w, a.runs, a.out, seed=a.seed, start=a.start)
+        txt = json.dumps(summ, indent=1)
+        if a.summary:
+            with open(a.summary, "w") as f:
+                f.write(txt)
+        print(json.dumps({"runs": summ["runs"], "headline": summ["headline"],
+                          "false_positives": summ["false_positives"]}))
+    else:
+        print(json.dumps(run_sweep(w, a.seeds, a.out, seed0=a.seed0, rho_every=a.rho_every)))
+
+
+if __name__ == "__main__":
+    main()

@@ -15,8 +15,11 @@ namespace {
 
 hipStream_t g_stream = nullptr;
 // Default relative threshold; a row is flagged when |r| > tau_rel * M + tau_abs
-// with M = sum_j |O_ij| + |pred_i|.
-float g_tau_rel = 1.0f / 4096.0f;
+// with M = sum_j |O_ij| + |pred_i|. 2^-16 is about 6.5x the largest fault-free
+// |r| / M seen on the benchmark workloads (2.3e-6) and about 7x below the
+// relative size of a single-element change of 2^-8 of the row's largest
+// output at d = 128.
+float g_tau_rel = 1.0f / 65536.0f;
 float g_tau_abs = 0.0f;
 
 constexpr float kLog2e = 1.4426950408889634f;

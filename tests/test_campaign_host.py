@@ -1,0 +1,101 @@
+"""Host-side tests of the fault campaign logic: fault draws respect the
+documented descriptor rules and cover every site and bit, classification
+follows the outcome definitions, and the summary arithmetic is right."""
+import json
+
+import numpy as np
+import pytest
+import torch
+
+import workloads as W
+from paper_2507_16676_amd import campaign as C
+
+W_C = W.WORKLOADS["dec_l4096"]
+
+
+def _valid(f, w, bc, qt):
+    off = w.Lk - w.Lq
+    assert 0 <= f.b < w.B and 0 <= f.h < w.H
+    if f.site in ("S", "P"):
+        assert 0 <= f.row < w.Lq and 0 <= f.col < w.Lk
+        assert not w.causal or f.col <= f.row + off
+        assert 0 <= f.bit < (32 if f.site == "S" else 16)
+    elif f.site == "O":
+        assert 0 <= f.row < w.Lq and 0 <= f.col < w.d and 0 <= f.bit < 32
+        last = min(w.Lk - 1, f.row + off) if w.causal else w.Lk - 1
+        assert 0 <= f.tile * bc <= last
+    else:
+        assert 0 <= f.row < w.Lk and 0 <= f.col < w.d and 0 <= f.bit < 16
+        n_qt = (w.Lq + qt - 1) // qt
+        assert 0 <= f.tile < n_qt
+        # some row of the query tile sees the key
+        last_row = min(w.Lq, (f.tile + 1) * qt) - 1
+        assert not w.causal or f.row <= last_row + off
+
+
+@pytest.mark.parametrize("w", [W_C, W.Workload("rect", 2, 3, 300, 77, 64, True, 0.125),
+                               W.Workload("nc", 1, 2, 100, 333, 128, False, 0.1)])
+def test_draws_are_valid_and_cover_sites_and_bits(w):
+    bc, qt = 64, 128
+    seen = set()
+    for r in range(3000):
+        f = C.draw_fault(r, w, bc, qt)
+        _valid(f, w, bc, qt)
+        seen.add((f.site, f.bit))
+    assert {s for s, _ in seen} == set(C.SITES)
+    for s in C.SITES:
+        assert {b for site, b in seen if site == s} == set(range(C.SITE_BITS[s]))
+
+
+def test_draws_are_reproducible():
+    a = [C.draw_fault(r, W_C, 64, 128) for r in range(50)]
+    b = [C.draw_fault(r, W_C, 64, 128) for r in range(50)]
+    assert a == b
+
+
+def test_classify_outcomes():
+    g = torch.randn(8, 16).to(torch.bfloat16)
+    none = torch.zeros(8, dtype=torch.uint8)
+    assert C.classify(g.clone(), g, none)["outcome"] == "benign"
+    o = g.clone()
+    o[3, 5] = o[3, 5] * 4 + 1                        # significant change in row 3
+    assert C.classify(o, g, none)["outcome"] == "silent"
+    fl = none.clone()
+    fl[3] = 1
+    r = C.classify(o, g, fl)
+    assert r["outcome"] == "detected" and r["rows_significant"] == 1
+    assert C.classify(g.clone(), g, fl)["outcome"] == "false_positive"
+    tiny = g.clone()
+    tiny[2, 0] = tiny[2, 0] + tiny[2].float().abs().max() * 2 ** -6 * 0.05   # < 2^-8 of row max
+    assert not torch.equal(tiny, g)
+    res = C.classify(tiny, g, none)
+    assert res["outcome"] == "benign"
+    fl2 = none.clone()
+    fl2[2] = 1
+    assert C.classify(tiny, g, fl2)["outcome"] == "detected_minor"
+    nan = g.clone()
+    nan[1, 1] = float("nan")
+    res = C.classify(nan, g, none)
+    assert res["outcome"] == "silent" and res["nonfinite"]
+
+
+def test_summary_counts(tmp_path):
+    recs = [
+        {"run": 0, "site": "O", "bit": 30, "exponent_bit": True, "outcome": "detected"},
+        {"run": 1, "site": "O", "bit": 2, "exponent_bit": False, "outcome": "benign"},
+        {"run": 2, "site": "P", "bit": 14, "exponent_bit": True, "outcome": "silent"},
+        {"run": 3, "site": "S", "bit": 30, "exponent_bit": True, "outcome": "silent"},
+        {"run": 4, "site": "V", "bit": 9, "exponent_bit": True, "outcome": "detected"},
+        {"run": 5, "site": "V", "bit": 15, "exponent_bit": False, "outcome": "false_positive"},
+    ]
+    p = tmp_path / "c.jsonl"
+    p.write_text("".join(json.dumps(r) + "\n" for r in recs))
+    s = C.summarize(str(p))
+    assert s["runs"] == 6
+    assert s["headline"]["detected"] == 2 and s["headline"]["silent"] == 1
+    assert s["headline"]["rate"] == pytest.approx(2 / 3)
+    lo, hi = s["headline"]["wilson95"]
+    assert lo < 2 / 3 < hi
+    assert s["false_positives"] == 1
+    assert s["per_site"]["S"]["silent"] == 1
+    assert s["per_bit"]["O30"]["detected"] == 1
