@@ -7,7 +7,7 @@
 
 namespace fabft {
 
-constexpr int kQueryTile = 128;  // query rows per workgroup
+constexpr int kQueryTile = 256;  // query rows per workgroup
 
 struct FwdParams {
   const uint16_t* q;

@@ -8,25 +8,33 @@
 // then O = o / l, pred = c / l (Eq. 8) and the per-row check against
 // actual = sum_j O_ij.
 //
-// Dataflow (one workgroup = 4 waves = 128 query rows; one wave = 32 rows):
+// Dataflow. One workgroup = 8 waves = 256 query rows (one workgroup per CU,
+// two waves per SIMD); one wave = 32 rows; key tiles of 64 keys.
 //  * The 32x32x16 bf16 MFMA computes S^T = K Q^T (keys on the M side, the
 //    wave's 32 queries on the N side) and O^T = V^T P^T. With this
 //    orientation a lane holds values of a single query row, so the row max,
 //    the sums l and c, the alpha rescale and the final row sum are in-lane
-//    work plus one exchange between lane i and lane i+32.
+//    work plus one exchange between lane i and lane i+32 (permlane32 swap).
 //  * Q stays in VGPRs as MFMA B operands for the whole pass.
-//  * K and V tiles are loaded with 16-byte global loads into registers two
-//    tiles ahead of use and written to a double-buffered LDS stage one tile
-//    ahead: K row-major (padded rows), V transposed (V^T, padded rows), so
-//    every MFMA A operand is one 16-byte LDS read. One barrier per tile.
+//  * K and V tiles go from global memory straight into a 4-stage LDS ring
+//    (global_load_lds_dwordx4: lane l of a load lands at base + 16 l), three
+//    tiles ahead of use, with no register staging. Both tiles are stored
+//    row-major with their 16-byte chunks XOR-swizzled by row: the K
+//    swizzle makes the MFMA operand reads conflict-free, the V swizzle makes
+//    the transposed reads conflict-free.
+//  * The V^T operand of the P V MFMA comes from row-major V through the
+//    transposing LDS read ds_read_b64_tr_b16: in a 16-lane group, lane r
+//    receives element r%4 of the 8-byte loads of lanes 4e + r/4 (e = 0..3);
+//    when lane 4e+q loads V[key0+e][col0+4q .. +3], lane r gets column
+//    col0+r of keys key0..key0+3, i.e. 4 k-slots of the MFMA A operand.
 //  * The K rows feeding MFMA row r are permuted (bits 2 and 3 of r swapped)
 //    so that the S^T accumulator of a lane already holds, for each 16-key
 //    step of P V, the 8 consecutive keys its B operand needs.
-//  * sumrow(V) of the tile is summed in fp32 from the loader's registers
-//    before V is written to LDS (the shared adder of the paper's checker),
-//    reduced across lanes with DPP, and stored for the tile as a bf16 pair
-//    hi + lo (hi = bf16(vs), lo = bf16(vs - hi); |vs - hi - lo| <= 2^-17|vs|)
-//    so that the checksum can use the packed bf16 dot product.
+//  * sumrow(V) of tile t+1 is computed from LDS by the whole workgroup while
+//    tile t is processed (8 threads per key, fp32 via v_dot2 and a DPP
+//    reduction) and stored as a bf16 pair hi + lo (hi = bf16(vs),
+//    lo = bf16(vs - hi); |vs - hi - lo| <= 2^-17|vs|): one sum per key and
+//    tile shared by the 256 rows, the paper's shared adder.
 //  * The weights p~ = bf16(p) feed the P V MFMA; l and the checksum c use
 //    exactly those p~ (v_dot2_f32_bf16 on the packed pairs), so that the
 //    rounding of P cancels between pred and actual. Every per-tile dot2
@@ -50,18 +58,18 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = 64 * kWaves;
 constexpr int kBr = 32 * kWaves;
+static_assert(kBr == kQueryTile, "query rows per workgroup");
+constexpr int kStages = 4;               // LDS ring depth (tiles in flight + 1)
+constexpr int kBc = 64;                  // keys per tile
 constexpr float kLazy = 8.0f;            // max drift (exp2 domain) before a rescale
 constexpr uint32_t kOnes = 0x3f803f80u;  // bf16 pair (1.0, 1.0)
-
-// BC keys per tile; the loader gives each thread KPT consecutive keys of one
-// 16-byte column chunk, so that it can write KPT-key runs of V^T.
-template <int D> struct TileCfg;
-template <> struct TileCfg<128> { static constexpr int BC = 64, KPT = 4; };
-template <> struct TileCfg<64> { static constexpr int BC = 64, KPT = 2; };
 
 __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -81,81 +89,76 @@ __device__ __forceinline__ float dpp(float x) {
       __builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over aligned groups of N consecutive lanes (N = 8 or 16); every lane
-// of the group receives the same value.
-template <int N>
-__device__ __forceinline__ float group_sum(float x) {
+// Sum over aligned groups of 8 consecutive lanes; every lane of the group
+// receives the same value.
+__device__ __forceinline__ float group8_sum(float x) {
   x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
   x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
   x += dpp<0x141>(x);  // row_half_mirror
-  if constexpr (N == 16) x += dpp<0x140>(x);  // row_mirror
   return x;
 }
 
 // Combine the values of lanes i and i ^ 32 with a symmetric operation:
 // v_permlane32_swap leaves (own, partner) in the two results of every lane.
 __device__ __forceinline__ float sum_xor32(float x) {
-#ifdef FABFT_SHFL_XOR32
-  return x + __shfl_xor(x, 32);
-#else
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-#endif
 }
 __device__ __forceinline__ float max_xor32(float x) {
-#ifdef FABFT_SHFL_XOR32
-  return __builtin_fmaxf(x, __shfl_xor(x, 32));
-#else
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __builtin_fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
-#endif
 }
 
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   f32x2 f = {a, b};
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
-__device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
-__device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
 // Row r of an MFMA 32-row block reads key 16*(r>>4) + 8*((r>>2)&1) + 4*((r>>3)&1) + (r&3)
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
 }
 
-// V^T row r keeps its 8-key (16-byte) chunks in the order c ^ ((r >> 4) & 7):
-// the loader's 8-byte writes (16 lanes on rows 8 apart) and the MFMA operand
-// reads (16 lanes on consecutive rows) then fall in distinct LDS banks.
-__device__ __forceinline__ int vt_chunk(int row, int c) { return c ^ ((row >> 4) & 7); }
+// s_waitcnt vmcnt(n) (expcnt and lgkmcnt left unconstrained), n < 16
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt(N | (0x7 << 4) | (0xF << 8));
+}
 
-// One LDS stage: a K tile, its V^T and sumrow(V) as bf16 hi/lo key pairs.
+// Tile layouts in LDS. A tile row (one key) holds D bf16 = CPR 16-byte
+// chunks; logical chunk c of row r is stored at chunk c ^ swz(r).
+template <int D>
+struct Tile {
+  static constexpr int CPR = D / 8;
+  // K: 16 lanes read 16 different rows at one logical chunk
+  static __device__ __forceinline__ int kswz(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+  // V: 32 lanes read 4 consecutive rows x 4 consecutive chunks
+  static __device__ __forceinline__ int vswz(int r) { return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); }
+  static __device__ __forceinline__ int kidx(int r, int c) { return r * D + 8 * (c ^ kswz(r)); }
+  static __device__ __forceinline__ int vidx(int r, int c) { return r * D + 8 * (c ^ vswz(r)); }
+};
+
 template <int D>
 struct Stage {
-  static constexpr int BC = TileCfg<D>::BC;
-  static constexpr int KST = D + 8;   // LDS row stride of K (elements)
-  static constexpr int VST = BC + 8;  // LDS row stride of V^T (elements)
-  uint16_t k[BC * KST];
-  uint16_t vt[D * VST];
-  uint32_t vs_hi[BC / 2];
-  uint32_t vs_lo[BC / 2];
+  uint16_t k[kBc * D];
+  uint16_t v[kBc * D];
+  uint16_t vs_hi[kBc];   // sumrow(V): bf16 hi part per key
+  uint16_t vs_lo[kBc];   // sumrow(V): bf16 lo part per key
 };
 
 template <int D, bool CAUSAL, bool CHECK, bool INJECT>
-#ifndef FABFT_MIN_BLOCKS
-#define FABFT_MIN_BLOCKS 2
-#endif
-__global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdParams p) {
-  constexpr int BC = TileCfg<D>::BC;
-  constexpr int KPT = TileCfg<D>::KPT;
-  constexpr int KST = Stage<D>::KST;
-  constexpr int VST = Stage<D>::VST;
-  constexpr int CPR = D / 8;      // 16-byte chunks per K/V row
+__global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
+  constexpr int BC = kBc;
+  constexpr int CPR = Tile<D>::CPR;
   constexpr int NKB = BC / 32;    // 32-key blocks per tile
   constexpr int NDB = D / 32;     // 32-column blocks of the output
   constexpr int NDS = D / 16;     // 16-wide steps over d in Q K^T
-  static_assert(kThreads == (BC / KPT) * CPR, "loader covers the tile");
+  constexpr int NLD = BC * CPR / kThreads;   // 16-byte loads per thread per tensor and tile
+  static_assert(NLD >= 1 && BC * CPR == NLD * kThreads, "loads cover the tile");
+  static_assert(kThreads == BC * 8 && CPR % 8 == 0, "sumrow: 8 threads per key");
 
-  __shared__ __attribute__((aligned(16))) Stage<D> stage[2];
+  __shared__ __attribute__((aligned(16))) Stage<D> stage[kStages];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -186,8 +189,10 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
   if (CAUSAL) kend = min(Lk, q0 + kBr + off);
   const int ntiles = kend > 0 ? (kend + BC - 1) / BC : 0;
 
-  // ---- Q fragments (B operand): lane holds query q0+32w+mrow, d slice 8*grp
-  const int qrow = q0 + 32 * wave + mrow;
+  const int wq_lo = q0 + 32 * wave;  // first query row of this wave
+  const int qrow = wq_lo + mrow;
+
+  // ---- Q fragments (B operand): lane holds query qrow, d slice 8*grp
   u32x4 qf[NDS];
 #pragma unroll
   for (int s = 0; s < NDS; ++s) {
@@ -204,136 +209,89 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
   float c_run = 0.f;
   const float sl2 = p.sl2;
 
-  // ---- loader: thread -> (16-byte chunk lc, group of KPT keys lkg)
-  const int lc = tid % CPR;
-  const int lkg = tid / CPR;
-  u32x4 kreg[KPT], vreg[KPT];
-  const size_t ld_off = kbase + (size_t)(KPT * lkg) * D + 8 * lc;
-  const uint16_t* kld = p.k + ld_off;   // this thread's first element of tile 0
-  const uint16_t* vld = p.v + ld_off;
-  auto gload = [&](int kv0) {
-    const size_t o = (size_t)kv0 * D;
-    if (kv0 + BC <= Lk) {   // whole tile in range (uniform)
+  // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
+  // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk repeat
+  // row Lk-1 (finite values that the mask gives weight 0)
+  const uint16_t* kg = p.k + kbase;
+  const uint16_t* vg = p.v + kbase;
+  auto issue = [&](int t) {
+    if (t >= ntiles) return;
+    Stage<D>& st = stage[t % kStages];
+    const int kv0 = t * BC;
 #pragma unroll
-      for (int r = 0; r < KPT; ++r) {
-        kreg[r] = *reinterpret_cast<const u32x4*>(kld + o + r * D);
-        vreg[r] = *reinterpret_cast<const u32x4*>(vld + o + r * D);
-      }
-    } else {
-#pragma unroll
-      for (int r = 0; r < KPT; ++r) {
-        kreg[r] = u32x4{0, 0, 0, 0};
-        vreg[r] = u32x4{0, 0, 0, 0};
-        if (kv0 + KPT * lkg + r < Lk) {
-          kreg[r] = *reinterpret_cast<const u32x4*>(kld + o + r * D);
-          vreg[r] = *reinterpret_cast<const u32x4*>(vld + o + r * D);
-        }
-      }
+    for (int j = 0; j < NLD; ++j) {
+      const int slot = j * kThreads + tid;
+      const int row = slot / CPR, sc = slot % CPR;
+      const int grow = min(kv0 + row, Lk - 1);
+      const uint16_t* ks = kg + (size_t)grow * D + 8 * (sc ^ Tile<D>::kswz(row));
+      const uint16_t* vsrc = vg + (size_t)grow * D + 8 * (sc ^ Tile<D>::vswz(row));
+      // each wave writes its own contiguous 1 KiB of the stage
+      const int wbase = (j * kThreads + 64 * wave) * 8;
+      __builtin_amdgcn_global_load_lds(ks, (lds_void*)(st.k + wbase), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(vsrc, (lds_void*)(st.v + wbase), 16, 0, 0);
     }
   };
 
-  // registers -> LDS stage `buf` for the tile starting at key kv0
-  auto stage_write = [&](int buf, int kv0) {
+  // ---- sumrow(V) of the tile in stage `buf` (Eq. 4): 8 threads per key
+  auto sumrow = [&](int buf, int t) {
     Stage<D>& st = stage[buf];
-    if constexpr (CHECK) {
-      // sumrow(V) of this thread's KPT keys (Eq. 4): its 8 values, then the
-      // CPR threads that share the keys
-      float vsum[KPT];
+    const int key = tid >> 3, part = tid & 7;
+    constexpr int CPT = CPR / 8;   // chunks per thread
+    float a = 0.f;
+    u32x4 ch[CPT];
 #pragma unroll
-      for (int r = 0; r < KPT; ++r) {
-        float a = dot2(vreg[r][0], kOnes, 0.f);
-        a = dot2(vreg[r][1], kOnes, a);
-        a = dot2(vreg[r][2], kOnes, a);
-        a = dot2(vreg[r][3], kOnes, a);
-        vsum[r] = group_sum<CPR>(a);
-      }
-      if (lc == 0) {
-        uint32_t hi[KPT / 2], lo[KPT / 2];
+    for (int i = 0; i < CPT; ++i) {
+      ch[i] = *reinterpret_cast<const u32x4*>(&st.v[Tile<D>::vidx(key, CPT * part + i)]);
 #pragma unroll
-        for (int r = 0; r < KPT / 2; ++r) {
-          hi[r] = pack_bf16x2(vsum[2 * r], vsum[2 * r + 1]);
-          lo[r] = pack_bf16x2(vsum[2 * r] - bf16_lo(hi[r]), vsum[2 * r + 1] - bf16_hi(hi[r]));
-        }
-        if constexpr (KPT == 4) {
-          *reinterpret_cast<u32x2*>(&st.vs_hi[2 * lkg]) = u32x2{hi[0], hi[1]};
-          *reinterpret_cast<u32x2*>(&st.vs_lo[2 * lkg]) = u32x2{lo[0], lo[1]};
-        } else {
-          st.vs_hi[lkg] = hi[0];
-          st.vs_lo[lkg] = lo[0];
-        }
-      }
+      for (int e = 0; e < 4; ++e) a = dot2(ch[i][e], kOnes, a);
+    }
+    const float vs = group8_sum(a);
+    if (part == 0) {
+      const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
+      const float hif = __uint_as_float(hi << 16);
+      const uint32_t lo = pack_bf16x2(vs - hif, 0.f) & 0xffffu;
+      st.vs_hi[key] = (uint16_t)hi;
+      st.vs_lo[key] = (uint16_t)lo;
     }
     if constexpr (INJECT) {
-      // V site: flip a bit of V[key][col] after sumrow was taken
-      if (p.f_site == 4 && bh == p.f_bh && qt == p.f_tile) {
-        const int fk = p.f_row - kv0 - KPT * lkg;
-        const int fc = p.f_col - 8 * lc;
-        if (fk >= 0 && fk < KPT && fc >= 0 && fc < 8) {
-          const uint32_t mask = (1u << p.f_bit) << (16 * (fc & 1));
+      // V site: flip a bit of V[key][col] of this workgroup's copy after
+      // sumrow read it (the thread that owns the chunk writes it back)
+      if (p.f_site == 4 && bh == p.f_bh && qt == p.f_tile && p.f_row - t * BC == key) {
+        const int c = p.f_col >> 3;
+        if (c / CPT == part) {
 #pragma unroll
-          for (int r = 0; r < KPT; ++r)
-            if (r == fk) {
+          for (int i = 0; i < CPT; ++i)
+            if (CPT * part + i == c) {
+              u32x4 w = ch[i];
+              const int e = (p.f_col & 7) >> 1;
+              const uint32_t mask = (1u << p.f_bit) << (16 * (p.f_col & 1));
 #pragma unroll
-              for (int e = 0; e < 4; ++e)
-                if (e == (fc >> 1)) vreg[r][e] ^= mask;
+              for (int ee = 0; ee < 4; ++ee)
+                if (ee == e) w[ee] ^= mask;
+              *reinterpret_cast<u32x4*>(&st.v[Tile<D>::vidx(key, c)]) = w;
             }
         }
       }
     }
-#pragma unroll
-    for (int r = 0; r < KPT; ++r)
-      *reinterpret_cast<u32x4*>(&st.k[(KPT * lkg + r) * KST + 8 * lc]) = kreg[r];
-    // V^T row 8lc+j, keys KPT*lkg .. +KPT-1: pairs of keys packed per dword
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const int e = j >> 1;
-      uint32_t w[KPT / 2];
-#pragma unroll
-      for (int r = 0; r < KPT / 2; ++r)
-        w[r] = (j & 1) == 0 ? (vreg[2 * r][e] & 0xffffu) | (vreg[2 * r + 1][e] << 16)
-                            : (vreg[2 * r][e] >> 16) | (vreg[2 * r + 1][e] & 0xffff0000u);
-      const int row = 8 * lc + j, key = KPT * lkg;
-      uint16_t* dst = &st.vt[row * VST + 8 * vt_chunk(row, key >> 3) + (key & 7)];
-      if constexpr (KPT == 4)
-        *reinterpret_cast<u32x2*>(dst) = u32x2{w[0], w[1]};
-      else
-        *reinterpret_cast<uint32_t*>(dst) = w[0];
-    }
   };
 
-  if (ntiles > 0) {
-    gload(0);
-    stage_write(0, 0);
-    if (ntiles > 1) gload(BC);
-  }
-
-  const int wq_lo = q0 + 32 * wave;  // first query row of this wave
-
-  for (int t = 0; t < ntiles; ++t) {
+  // ---- one key tile for this wave (steps A1-A5)
+  auto compute = [&](int t) {
+    const Stage<D>& st = stage[t % kStages];
     const int kv0 = t * BC;
-    // tile t sits in stage t&1; every wave is done with tile t-1, whose
-    // stage (t+1)&1 is refilled with tile t+1
-    __syncthreads();
-    if (t + 1 < ntiles) {
-      stage_write((t + 1) & 1, kv0 + BC);
-      if (t + 2 < ntiles) gload(kv0 + 2 * BC);
-    }
-    const Stage<D>& st = stage[t & 1];
-
-    // waves whose rows see none of this tile's keys skip it
-    if (CAUSAL && kv0 > wq_lo + 31 + off) continue;
     const bool need_mask = (kv0 + BC > Lk) || (CAUSAL && kv0 + BC - 1 > wq_lo + off);
 
-    // ---- S^T = K Q^T (Alg. 3: s_i = q . k_i)
+    // S^T = K Q^T (Alg. 3: s_i = q . k_i)
     f32x16 sacc[NKB];
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) sacc[kb] = f32x16{};
+    const int krow = swap_bits23(mrow);
 #pragma unroll
     for (int s = 0; s < NDS; ++s) {
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
         const u32x4 a = *reinterpret_cast<const u32x4*>(
-            &st.k[(kb * 32 + swap_bits23(mrow)) * KST + 16 * s + 8 * grp]);
+            &st.k[Tile<D>::kidx(kb * 32 + krow, 2 * s + grp)]);
         sacc[kb] = mfma32(a, qf[s], sacc[kb]);
       }
     }
@@ -353,7 +311,7 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
       }
     }
 
-    // ---- mask, tile max (Alg. 3: m_i = max(m_{i-1}, s_i))
+    // mask, tile max (Alg. 3: m_i = max(m_{i-1}, s_i))
     if (need_mask) {
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
@@ -378,7 +336,7 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
     m2_run = m2_new;
     const float nm2 = (m2_new == -__builtin_inff()) ? 0.f : -m2_new;
 
-    // ---- p = exp(s - m) and p~ = bf16(p), the B operands of P V
+    // p = exp(s - m) and p~ = bf16(p), the B operands of P V
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
@@ -403,7 +361,7 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
         for (int e = 0; e < 4; ++e)
           pb[kb][h][e] = pack_bf16x2(sacc[kb][8 * h + 2 * e], sacc[kb][8 * h + 2 * e + 1]);
 
-    // ---- l = l*alpha + sum p~ (Alg. 3)
+    // l = l*alpha + sum p~ (Alg. 3)
     float lsum = 0.f;
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
@@ -413,16 +371,16 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
         for (int e = 0; e < 4; ++e) lsum = dot2(pb[kb][h][e], kOnes, lsum);
     l_run = __builtin_fmaf(l_run, alpha, lsum);
 
-    // ---- online checksum (Alg. 3: c = c*alpha + sumrow(V) * p~)
+    // online checksum (Alg. 3: c = c*alpha + sumrow(V) * p~)
     if constexpr (CHECK) {
       float csum = 0.f;
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
         for (int h = 0; h < 2; ++h) {
-          const int pi = 16 * kb + 8 * h + 4 * grp;  // first key pair of this lane
-          const u32x4 vh = *reinterpret_cast<const u32x4*>(&st.vs_hi[pi]);
-          const u32x4 vl = *reinterpret_cast<const u32x4*>(&st.vs_lo[pi]);
+          const int k0 = 32 * kb + 16 * h + 8 * grp;  // first key of this lane's 8
+          const u32x4 vh = *reinterpret_cast<const u32x4*>(&st.vs_hi[k0]);
+          const u32x4 vl = *reinterpret_cast<const u32x4*>(&st.vs_lo[k0]);
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             csum = dot2(pb[kb][h][e], vh[e], csum);
@@ -448,23 +406,34 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
       }
     }
 
-    // ---- O^T = alpha O^T + V^T P^T (Alg. 3: o = o*alpha + v * p)
+    // O^T = alpha O^T + V^T P^T (Alg. 3: o = o*alpha + v * p)
     if (__ballot(alpha != 1.f)) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
     }
-    // (output blocks innermost: consecutive MFMAs accumulate independently)
+    // transposed reads: 16-lane group G = lane/16, lane L = 4e + q in it reads
+    // V[32kb + 16h + 8(G>>1) + 4t + e][32db + 16(G&1) + 4q .. +3]
+    const int gq = lane >> 4, ll = lane & 15;
+    const int tr_key = 8 * (gq >> 1) + (ll >> 2);
+    const int tr_col = 16 * (gq & 1) + 4 * (ll & 3);
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
         for (int db = 0; db < NDB; ++db) {
-          const int row = 32 * db + mrow;
-          const u32x4 a = *reinterpret_cast<const u32x4*>(
-              &st.vt[row * VST + 8 * vt_chunk(row, 4 * kb + 2 * h + grp)]);
+          u32x2 part[2];
+#pragma unroll
+          for (int t2 = 0; t2 < 2; ++t2) {
+            const int key = 32 * kb + 16 * h + 4 * t2 + tr_key;
+            const int col = 32 * db + tr_col;
+            const int idx = Tile<D>::vidx(key, col >> 3) + (col & 7);
+            const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st.v + idx));
+            part[t2] = __builtin_bit_cast(u32x2, r);
+          }
+          const u32x4 a = {part[0][0], part[0][1], part[1][0], part[1][1]};
           oacc[db] = mfma32(a, pb[kb][h], oacc[db]);
         }
     if constexpr (INJECT) {
@@ -483,6 +452,33 @@ __global__ __launch_bounds__(kThreads, FABFT_MIN_BLOCKS) void fwd_kernel(FwdPara
         }
       }
     }
+  };
+
+  // ---- pipeline: tiles t+1 and t+2 in flight while tile t is processed
+  constexpr int LPT = 2 * NLD;   // loads per thread per tile (K and V)
+  if (ntiles > 0) {
+    issue(0);
+    issue(1);
+    issue(2);
+    // tile 0 complete; tiles 1 and 2 may be outstanding
+    if (ntiles >= 3) wait_vmcnt<2 * LPT>();
+    else if (ntiles == 2) wait_vmcnt<LPT>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    if constexpr (CHECK) sumrow(0, 0);
+  }
+  for (int t = 0; t < ntiles; ++t) {
+    // tile t+1 complete (tile t+2 may still be in flight); after the barrier
+    // every wave is done with tile t-1, whose stage takes tile t+3
+    if (t + 2 < ntiles) wait_vmcnt<LPT>();
+    else wait_vmcnt<0>();
+    __syncthreads();
+    issue(t + 3);
+    if constexpr (CHECK) {
+      if (t + 1 < ntiles) sumrow((t + 1) % kStages, t + 1);
+    }
+    // waves whose rows see none of this tile's keys skip it
+    if (!CAUSAL || t * BC <= wq_lo + 31 + off) compute(t);
   }
 
   // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
@@ -557,6 +553,6 @@ int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t str
   return launch_d<64>(p, causal, mode, stream);
 }
 
-int key_tile(int d) { return d == 128 ? TileCfg<128>::BC : TileCfg<64>::BC; }
+int key_tile(int d) { return (d == 64 || d == 128) ? kBc : 0; }
 
 }  // namespace fabft

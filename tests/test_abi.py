@@ -40,7 +40,7 @@ def test_status_strings():
 def test_key_and_query_tiles():
     assert F.key_tile(128) == 64
     assert F.key_tile(64) == 64
-    assert F.query_tile() == 128
+    assert F.query_tile() == 256
     with pytest.raises(F.FabftError):
         F.key_tile(96)
 

@@ -78,14 +78,16 @@ def test_p_site_flip(golden):
 
 
 def test_v_site_flip(golden):
-    # key 100, column 5, in the workgroup holding query rows 128..255
+    # key 100, column 5, in the workgroup holding the second query tile
+    qt = F.query_tile()
+    lo, hi = qt, min(2 * qt, W_INJ.Lq)
     f = F.Fault("V", b=0, h=1, row=100, col=5, tile=1, bit=14)
     o, resid, flags, pred, actual = _inject(golden, f)
     (_, (o0, r0, f0, p0, a0)) = golden
     changed = _changed_rows(o, o0)
-    assert changed and all(h == 1 and 128 <= i < 256 for _, h, i in changed)
+    assert changed and all(h == 1 and lo <= i < hi for _, h, i in changed)
     flagged = set(map(tuple, (flags != 0).nonzero().cpu().numpy().tolist()))
-    assert flagged and flagged <= {(0, 1, i) for i in range(128, 256)}
+    assert flagged and flagged <= {(0, 1, i) for i in range(lo, hi)}
     # every row whose output moved by more than 2^-8 of its max is flagged
     O = G.from_dev_bf16(o)[0, 1]
     O0 = G.from_dev_bf16(o0)[0, 1]
