@@ -36,10 +36,11 @@
 //    lo = bf16(vs - hi); |vs - hi - lo| <= 2^-17|vs|): one sum per key and
 //    tile shared by the 256 rows, the paper's shared adder.
 //  * The weights p~ = bf16(p) feed the P V MFMA; l and the checksum c use
-//    exactly those p~ (v_dot2_f32_bf16 on the packed pairs), so that the
-//    rounding of P cancels between pred and actual. Every per-tile dot2
-//    chain starts from zero and is folded into the running l and c with an
-//    ordinary fp32 multiply-add.
+//    exactly those p~, so that the rounding of P cancels between pred and
+//    actual. They come from one more 32x32x16 MFMA per 16-key step with the
+//    same P^T operand and a 4-row A operand [sumrow hi; sumrow lo; ones; 0]
+//    held in LDS: rows 0-2 of that accumulator are c_hi, c_lo and l of each
+//    query, rescaled like o (Eq. 10 carries c as an extra row of V^T).
 //  * Lazy rescaling: the running max used for the exponentials is moved only
 //    when a tile's max exceeds it by more than 8 in the exp2 domain, so
 //    p <= 256 and o, l, c are rescaled (alpha != 1) rarely; o*alpha is
@@ -139,12 +140,15 @@ struct Tile {
   static __device__ __forceinline__ int vidx(int r, int c) { return r * D + 8 * (c ^ vswz(r)); }
 };
 
+// Rows of the small A operand that yields c and l: sumrow(V) as bf16 hi and
+// lo parts, ones, zeros (MFMA rows >= 3 read the zero row).
+enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3 };
+
 template <int D>
 struct Stage {
   uint16_t k[kBc * D];
   uint16_t v[kBc * D];
-  uint16_t vs_hi[kBc];   // sumrow(V): bf16 hi part per key
-  uint16_t vs_lo[kBc];   // sumrow(V): bf16 lo part per key
+  uint16_t vsm[4][kBc];
 };
 
 template <int D, bool CAUSAL, bool CHECK, bool INJECT>
@@ -204,10 +208,18 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   f32x16 oacc[NDB];
 #pragma unroll
   for (int b = 0; b < NDB; ++b) oacc[b] = f32x16{};
+  f32x16 aux = {};                    // lanes < 32: [0] c_hi, [1] c_lo, [2] l of query mrow
   float m2_run = -__builtin_inff();   // running max, exp2 domain (s * scale * log2 e)
-  float l_run = 0.f;
-  float c_run = 0.f;
   const float sl2 = p.sl2;
+
+  // constant rows of the c / l operand in every stage (visible after the
+  // prologue barrier)
+  {
+    const int st_i = tid >> 7, row = kRowOnes + ((tid >> 6) & 1), key = tid & 63;
+    stage[st_i].vsm[row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
+  }
+  // MFMA row of this lane in the c / l operand (rows 0, 1 only with the checksum)
+  const int vsm_row = (mrow < 2 && !CHECK) ? kRowZero : min(mrow, (int)kRowZero);
 
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
   // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk repeat
@@ -250,8 +262,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
       const float hif = __uint_as_float(hi << 16);
       const uint32_t lo = pack_bf16x2(vs - hif, 0.f) & 0xffffu;
-      st.vs_hi[key] = (uint16_t)hi;
-      st.vs_lo[key] = (uint16_t)lo;
+      st.vsm[kRowVsHi][key] = (uint16_t)hi;
+      st.vsm[kRowVsLo][key] = (uint16_t)lo;
     }
     if constexpr (INJECT) {
       // V site: flip a bit of V[key][col] of this workgroup's copy after
@@ -361,34 +373,23 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
         for (int e = 0; e < 4; ++e)
           pb[kb][h][e] = pack_bf16x2(sacc[kb][8 * h + 2 * e], sacc[kb][8 * h + 2 * e + 1]);
 
-    // l = l*alpha + sum p~ (Alg. 3)
-    float lsum = 0.f;
+    // c = c*alpha + sumrow(V) p~ and l = l*alpha + sum p~ (Alg. 3): the
+    // c / l MFMA reads p~ before the P site and the P V product
+    if (__ballot(alpha != 1.f)) {
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) aux[i] *= alpha;
+    }
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) lsum = dot2(pb[kb][h][e], kOnes, lsum);
-    l_run = __builtin_fmaf(l_run, alpha, lsum);
-
-    // online checksum (Alg. 3: c = c*alpha + sumrow(V) * p~)
-    if constexpr (CHECK) {
-      float csum = 0.f;
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int k0 = 32 * kb + 16 * h + 8 * grp;  // first key of this lane's 8
-          const u32x4 vh = *reinterpret_cast<const u32x4*>(&st.vs_hi[k0]);
-          const u32x4 vl = *reinterpret_cast<const u32x4*>(&st.vs_lo[k0]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            csum = dot2(pb[kb][h][e], vh[e], csum);
-            csum = dot2(pb[kb][h][e], vl[e], csum);
-          }
-        }
-      c_run = __builtin_fmaf(c_run, alpha, csum);
-    }
+      for (int h = 0; h < 2; ++h) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(&st.vsm[vsm_row][32 * kb + 16 * h + 8 * grp]);
+        aux = mfma32(a, pb[kb][h], aux);
+      }
     if constexpr (INJECT) {
       if (p.f_site == 2 && bh == p.f_bh && qrow == p.f_row) {
         const int kl = p.f_col - kv0;
@@ -406,13 +407,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       }
     }
 
-    // O^T = alpha O^T + V^T P^T (Alg. 3: o = o*alpha + v * p)
-    if (__ballot(alpha != 1.f)) {
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-    }
+    // O^T = alpha O^T + V^T P^T (Alg. 3: o = o*alpha + v * p); o was
+    // rescaled above
     // transposed reads: 16-lane group G = lane/16, lane L = 4e + q in it reads
     // V[32kb + 16h + 8(G>>1) + 4t + e][32db + 16(G&1) + 4q .. +3]
     const int gq = lane >> 4, ll = lane & 15;
@@ -482,7 +478,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   }
 
   // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
-  const float l_tot = sum_xor32(l_run);
+  const float l_tot = sum_xor32(aux[2]);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
   float act = 0.f, absum = 0.f;
 #pragma unroll
@@ -508,7 +504,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   if constexpr (CHECK) {
     act = sum_xor32(act);
     absum = sum_xor32(absum);
-    const float c_tot = sum_xor32(c_run);
+    const float c_tot = sum_xor32(aux[0] + aux[1]);
     const float pred = c_tot * inv;
     const float r = pred - act;
     const float M = absum + __builtin_fabsf(pred);
