@@ -180,9 +180,10 @@ def main():
     ratios.sort()
     overhead = 100.0 * (ratios[len(ratios) // 2] - 1.0)
     ms_off = sorted(off_ms)[len(off_ms) // 2]
+    ms_on_r = sorted(on_ms)[len(on_ms) // 2]
     tflops_off = flops / (ms_off * 1e-3) / 1e12
     log(f"[bench] checksum off: {ms_off:.4f} ms/step, {tflops_off:.1f} TFLOP/s; "
-        f"overhead {overhead:.2f}%")
+        f"interleaved on {ms_on_r:.4f} ms/step; overhead {overhead:.2f}%")
 
     # ---- roofline of the dominant kernel (the checksum-on forward)
     achieved = flops / (avg_launch_ms * 1e-3) / 1e12

@@ -127,6 +127,17 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt(N | (0x7 << 4) | (0xF << 8));
 }
 
+// global_load_lds_dwordx4 as inline asm: the 16 bytes at gptr of lane l land
+// at LDS address lds + 16 l (lds is wave-uniform and goes through m0). The
+// compiler does not see this load, so it adds no wait of its own before LDS
+// reads: its tracking of the builtin form makes every transposed V read wait
+// for all outstanding loads, the prefetched tiles included. wait_vmcnt and
+// the workgroup barrier are what order these loads before their readers.
+__device__ __forceinline__ void load_lds16(const void* gptr, lds_void* lds) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(base) : "memory");
+}
+
 // Tile layouts in LDS. A tile row (one key) holds D bf16 = CPR 16-byte
 // chunks; logical chunk c of row r is stored at chunk c ^ swz(r).
 template <int D>
@@ -191,7 +202,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 
   int kend = Lk;
   if (CAUSAL) kend = min(Lk, q0 + kBr + off);
-  const int ntiles = kend > 0 ? (kend + BC - 1) / BC : 0;
+  // wave-uniform (the division runs on the vector ALU): scalar branches
+  const int ntiles = __builtin_amdgcn_readfirstlane(kend > 0 ? (kend + BC - 1) / BC : 0);
 
   const int wq_lo = q0 + 32 * wave;  // first query row of this wave
   const int qrow = wq_lo + mrow;
@@ -239,8 +251,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       const uint16_t* vsrc = vg + (size_t)grow * D + 8 * (sc ^ Tile<D>::vswz(row));
       // each wave writes its own contiguous 1 KiB of the stage
       const int wbase = (j * kThreads + 64 * wave) * 8;
-      __builtin_amdgcn_global_load_lds(ks, (lds_void*)(st.k + wbase), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(vsrc, (lds_void*)(st.v + wbase), 16, 0, 0);
+      load_lds16(ks, (lds_void*)(st.k + wbase));
+      load_lds16(vsrc, (lds_void*)(st.v + wbase));
     }
   };
 
@@ -463,6 +475,11 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     __syncthreads();
     if constexpr (CHECK) sumrow(0, 0);
   }
+  // A use of Q here, on every path into the loop, puts the compiler's own
+  // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
+  // also waits for tiles 1 and 2) before the loop rather than inside it.
+#pragma unroll
+  for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
   for (int t = 0; t < ntiles; ++t) {
     // tile t+1 complete (tile t+2 may still be in flight); after the barrier
     // every wave is done with tile t-1, whose stage takes tile t+3
