@@ -181,18 +181,29 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   const int mrow = lane & 31;   // MFMA row / column index of this lane
   const int grp = lane >> 5;    // which 8-wide k slice this lane holds
 
-  // ---- workgroup -> (head, query tile): keep each head on one XCD, the
-  // heaviest causal tiles first
+  // ---- workgroup -> (head, query tile). Workgroups go to the 8 XCDs round
+  // robin (XCD = id mod 8). Without a mask every tile costs the same: each
+  // XCD takes a contiguous range of heads, so that a head's K and V stay in
+  // one L2. With the causal mask the work per query tile grows with its
+  // index: all heads' heaviest tiles go first (longest job first); with a
+  // head count divisible by 8 a head still stays on one XCD.
   const int G = p.grid;
   const int bid = blockIdx.x;
-  const int xcd = bid & 7;
-  const int per = G >> 3, rem = G & 7;
-  const int slot = bid >> 3;
-  const int logical = (xcd < rem) ? xcd * (per + 1) + slot
-                                  : rem * (per + 1) + (xcd - rem) * per + slot;
-  const int bh = logical / p.n_qt;
-  int qt = logical - bh * p.n_qt;
-  if (CAUSAL) qt = p.n_qt - 1 - qt;
+  int bh, qt;
+  if (CAUSAL) {
+    const int BH = G / p.n_qt;
+    const int qr = bid / BH;
+    bh = bid - qr * BH;
+    qt = p.n_qt - 1 - qr;
+  } else {
+    const int xcd = bid & 7;
+    const int per = G >> 3, rem = G & 7;
+    const int slot = bid >> 3;
+    const int logical = (xcd < rem) ? xcd * (per + 1) + slot
+                                    : rem * (per + 1) + (xcd - rem) * per + slot;
+    bh = logical / p.n_qt;
+    qt = logical - bh * p.n_qt;
+  }
 
   const int Lq = p.Lq, Lk = p.Lk;
   const int q0 = qt * kBr;
@@ -310,15 +321,23 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb) sacc[kb] = f32x16{};
     const int krow = swap_bits23(mrow);
+    // operand reads run KAHEAD MFMAs ahead of their use (the scheduling
+    // barriers keep the compiler from pulling them back next to the MFMA)
+    constexpr int NQK = NDS * NKB, KAHEAD = 6;
+    auto kread = [&](int i) {
+      return *reinterpret_cast<const u32x4*>(
+          &st.k[Tile<D>::kidx((i % NKB) * 32 + krow, 2 * (i / NKB) + grp)]);
+    };
+    u32x4 kop[NQK];
 #pragma unroll
-    for (int s = 0; s < NDS; ++s) {
+    for (int i = 0; i < KAHEAD; ++i) kop[i] = kread(i);
 #pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(
-            &st.k[Tile<D>::kidx(kb * 32 + krow, 2 * s + grp)]);
-        sacc[kb] = mfma32(a, qf[s], sacc[kb]);
-      }
+    for (int i = 0; i < NQK; ++i) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + KAHEAD < NQK) kop[i + KAHEAD] = kread(i + KAHEAD);
+      sacc[i % NKB] = mfma32(kop[i], qf[i / NKB], sacc[i % NKB]);
     }
+    __builtin_amdgcn_sched_barrier(0);
     // accumulator element i of block kb holds key kv0 + 32kb + 16(i/8) + 8grp + (i%8)
     if constexpr (INJECT) {
       if (p.f_site == 1 && bh == p.f_bh && qrow == p.f_row) {
@@ -426,24 +445,32 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     const int gq = lane >> 4, ll = lane & 15;
     const int tr_key = 8 * (gq >> 1) + (ll >> 2);
     const int tr_col = 16 * (gq & 1) + 4 * (ll & 3);
+    // step i = (kb, h, db); its two transposed reads run VAHEAD steps ahead
+    constexpr int NPV = NKB * 2 * NDB, VAHEAD = 4;
+    auto vread = [&](int i) {
+      const int kb = i / (2 * NDB), h = (i / NDB) % 2, db = i % NDB;
+      u32x2 part[2];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
+      for (int t2 = 0; t2 < 2; ++t2) {
+        const int key = 32 * kb + 16 * h + 4 * t2 + tr_key;
+        const int col = 32 * db + tr_col;
+        const int idx = Tile<D>::vidx(key, col >> 3) + (col & 7);
+        const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st.v + idx));
+        part[t2] = __builtin_bit_cast(u32x2, r);
+      }
+      return u32x4{part[0][0], part[0][1], part[1][0], part[1][1]};
+    };
+    u32x4 vop[NPV];
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
+    for (int i = 0; i < VAHEAD; ++i) vop[i] = vread(i);
 #pragma unroll
-        for (int db = 0; db < NDB; ++db) {
-          u32x2 part[2];
-#pragma unroll
-          for (int t2 = 0; t2 < 2; ++t2) {
-            const int key = 32 * kb + 16 * h + 4 * t2 + tr_key;
-            const int col = 32 * db + tr_col;
-            const int idx = Tile<D>::vidx(key, col >> 3) + (col & 7);
-            const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st.v + idx));
-            part[t2] = __builtin_bit_cast(u32x2, r);
-          }
-          const u32x4 a = {part[0][0], part[0][1], part[1][0], part[1][1]};
-          oacc[db] = mfma32(a, pb[kb][h], oacc[db]);
-        }
+    for (int i = 0; i < NPV; ++i) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (i + VAHEAD < NPV) vop[i + VAHEAD] = vread(i + VAHEAD);
+      const int kb = i / (2 * NDB), h = (i / NDB) % 2, db = i % NDB;
+      oacc[db] = mfma32(vop[i], pb[kb][h], oacc[db]);
+    }
+    __builtin_amdgcn_sched_barrier(0);
     if constexpr (INJECT) {
       // O site: accumulator element (row, col) after the P V of tile f_tile
       if (p.f_site == 3 && bh == p.f_bh && qrow == p.f_row && t == p.f_tile) {
@@ -486,12 +513,12 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     if (t + 2 < ntiles) wait_vmcnt<LPT>();
     else wait_vmcnt<0>();
     __syncthreads();
+    if (!CAUSAL || t * BC <= wq_lo + 31 + off) compute(t);
     issue(t + 3);
     if constexpr (CHECK) {
       if (t + 1 < ntiles) sumrow((t + 1) % kStages, t + 1);
     }
-    // waves whose rows see none of this tile's keys skip it
-    if (!CAUSAL || t * BC <= wq_lo + 31 + off) compute(t);
+
   }
 
   // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
