@@ -121,6 +121,8 @@ def main():
     ap.add_argument("--rounds", type=int, default=5,
                     help="interleaved on/off rounds for the overhead figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--weighted", action="store_true",
+                    help="also run the weighted second checksum (an extension)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one plain device copy of this size (calibrates "
@@ -135,6 +137,7 @@ def main():
 
     import torch
     import paper_2507_16676_amd as F
+    F.set_weighted_check(args.weighted)
     import workloads as W
 
     w = W.WORKLOADS[args.workload]
@@ -225,7 +228,8 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic (seeded N(0,1), drawn on the GPU)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "Lq": w.Lq, "Lk": w.Lk,
-                   "d": w.d, "causal": w.causal, "scale": w.scale, "checksum": "on"},
+                   "d": w.d, "causal": w.causal, "scale": w.scale,
+                   "checksum": "on+weighted" if args.weighted else "on"},
         "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "checksum_off": {"ms_per_step": round(ms_off, 5), "tflops": round(tflops_off, 2)},
         "checksum_overhead_pct": round(overhead, 3),

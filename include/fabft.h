@@ -18,8 +18,8 @@
  *    16-byte aligned. resid is fp32 [B, H, Lq], flags is uint8 [B, H, Lq],
  *    pred/actual (when given) fp32 [B, H, Lq]; all device pointers.
  *  - The caller owns every buffer. The library allocates nothing and keeps
- *    only a stream and the detection threshold as process-global state
- *    (setters are not thread-safe).
+ *    only a stream, the detection threshold and the weighted-check switch as
+ *    process-global state (setters are not thread-safe).
  *  - d must be 64 or 128. B, H, Lq, Lk >= 1. scale must be finite and >= 0.
  *  - causal != 0 keeps key k for query i iff k <= i + (Lk - Lq)
  *    (bottom-right aligned; the plain lower triangle when Lq == Lk). A query
@@ -57,9 +57,12 @@ enum {
 
 /* Detection flags, one byte per query row. */
 enum {
-  FABFT_FLAG_RESID = 1,    /* |pred - actual| > tau_rel * M + tau_abs, where
-                              M = sum_j |O_ij| + |pred| */
-  FABFT_FLAG_NONFINITE = 2 /* the residual is NaN or infinite */
+  FABFT_FLAG_RESID = 1,     /* |pred - actual| > tau_rel * M + tau_abs, where
+                               M = sum_j |O_ij| + |pred| */
+  FABFT_FLAG_NONFINITE = 2, /* a residual is NaN or infinite */
+  FABFT_FLAG_WEIGHTED = 4   /* weighted check only (fabft_set_weighted_check):
+                               |pred_w - actual_w| > tau_rel * M_w + tau_abs,
+                               M_w = sum_j |O_ij| + |pred_w| */
 };
 
 /*
@@ -92,6 +95,20 @@ void fabft_set_stream(void* hip_stream);
  */
 int fabft_set_threshold(float tau_rel, float tau_abs);
 void fabft_get_threshold(float* tau_rel, float* tau_abs);
+
+/*
+ * Second, weighted checksum (an extension beyond the paper, which uses one
+ * checksum per row): with on != 0, every checksum-on launch also carries
+ *   c_w <- c_w * exp(m_old - m_new) + (sum_j (-1)^j V_kj) * p~_k
+ * and compares pred_w = c_w / l with actual_w = sum_j (-1)^j O_ij, the same
+ * way as the paper's check (flag FABFT_FLAG_WEIGHTED). A fault on p~_k after
+ * the checksum read it moves actual by delta * sumrow_k(V) / l, which the
+ * paper's check misses when sumrow_k(V) is near 0; the weighted sum of that
+ * V row is then usually far from 0. Default: off. Process-global, not
+ * thread-safe. resid stays the paper's residual pred - actual.
+ */
+void fabft_set_weighted_check(int on);
+int fabft_get_weighted_check(void);
 
 /* Number of keys per key tile of the kernel for head dimension d (the unit
  * of fabft_fault.tile at the O site), or FABFT_E_HEADDIM. */
@@ -131,15 +148,18 @@ typedef struct {
 /*
  * Debug / fault-injection variant of fabft_attn_fwd (a separate kernel
  * instantiation; the production kernels carry no injection code).
- * f may be NULL (same as site NONE). pred and actual may be NULL; when
- * given, they receive c/l and sum_j O_ij per row (fp32 [B, H, Lq]).
- * Returns FABFT_E_FAULT if the descriptor is out of range. Asynchronous.
+ * f may be NULL (same as site NONE). pred, actual, pred_w and actual_w may
+ * be NULL; when given, they receive c/l and sum_j O_ij per row, and with the
+ * weighted check on, c_w/l and sum_j (-1)^j O_ij (0 when it is off); all
+ * fp32 [B, H, Lq]. Returns FABFT_E_FAULT if the descriptor is out of range.
+ * Asynchronous.
  */
 int fabft_attn_fwd_inject(const void* q, const void* k, const void* v,
                           void* o, float* resid, uint8_t* flags,
                           int B, int H, int Lq, int Lk, int d, int causal,
                           float scale, const fabft_fault* f,
-                          float* pred, float* actual);
+                          float* pred, float* actual,
+                          float* pred_w, float* actual_w);
 
 /* Human-readable text for a status code (static storage). */
 const char* fabft_status_str(int status);

@@ -19,6 +19,11 @@ What it computes, per head and per query row i (Section III-A):
                                                    without reading O)
   actual_i = sum_j O_ij,  resid_i = pred_i - actual_i
 
+and, as an extension beyond the paper (a classic weighted ABFT checksum
+next to the paper's plain one), for weights w_j (default (-1)^j):
+
+  pred_w_i = sum_k p_ik (sum_j w_j V_kj) / l_i,   actual_w_i = sum_j w_j O_ij
+
 plus the global check of Eq. 5 from the explicit column sums of the
 normalised score matrix (Eq. 3), and fp64 restatements of Algorithm 1
 (attention with lazy softmax division, two passes over the keys) and
@@ -45,7 +50,7 @@ import numpy as np
 __all__ = [
     "visible_mask", "sumrow", "attention_head", "attention",
     "global_check", "lazy_softmax_attention", "online_checksum_attention",
-    "threshold_flags",
+    "threshold_flags", "alternating_weights", "weighted_check_head",
 ]
 
 
@@ -90,6 +95,38 @@ def attention_head(q, k, v, causal: bool, scale: float, rows=None) -> dict:
     actual = O.sum(axis=1)
     return {"O": O, "pred": pred, "actual": actual, "resid": pred - actual,
             "l": l, "m": m}
+
+
+def alternating_weights(d: int) -> np.ndarray:
+    """w_j = (-1)^j, j = 0 .. d-1."""
+    return np.where(np.arange(d) % 2 == 0, 1.0, -1.0)
+
+
+def weighted_check_head(q, k, v, causal: bool, scale: float, w=None, rows=None) -> dict:
+    """Weighted checksum of one head (not in the paper): the plain definition
+    of pred_w = sum_k p_ik (sum_j w_j V_kj) / l_i, built without reading O,
+    and of actual_w = sum_j w_j O_ij. w defaults to (-1)^j; w = 1 gives the
+    paper's check (Eq. 8). Returns fp64 arrays pred_w, actual_w, resid_w.
+    """
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    v = np.asarray(v, dtype=np.float64)
+    d = v.shape[1]
+    w = alternating_weights(d) if w is None else np.asarray(w, dtype=np.float64)
+    Lq, Lk = q.shape[0], k.shape[0]
+    rows = np.arange(Lq) if rows is None else np.asarray(rows)
+    s = scale * (q[rows] @ k.T)
+    vis = visible_mask(Lq, Lk, causal, rows)
+    s = np.where(vis, s, -np.inf)
+    any_vis = vis.any(axis=1)
+    m = np.where(any_vis, s.max(axis=1), 0.0)
+    p = np.where(vis, np.exp(s - m[:, None]), 0.0)
+    l_safe = np.where(any_vis, p.sum(axis=1), 1.0)
+    vw = v @ w                                        # weighted row sums of V
+    pred_w = (p @ vw) / l_safe
+    O = (p @ v) / l_safe[:, None]
+    actual_w = O @ w
+    return {"pred_w": pred_w, "actual_w": actual_w, "resid_w": pred_w - actual_w}
 
 
 def attention(q, k, v, causal: bool, scale: float, rows=None,

@@ -28,7 +28,7 @@ _fp = ctypes.POINTER(ctypes.c_float)
 FABFT_OK = 0
 E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD = \
     -1, -2, -3, -4, -5, -6, -7, -8
-FLAG_RESID, FLAG_NONFINITE = 1, 2
+FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED = 1, 2, 4
 SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V = 0, 1, 2, 3, 4
 SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V}
 
@@ -50,13 +50,18 @@ def _load() -> ctypes.CDLL:
         raise ImportError(
             f"{LIB_PATH} is not built; run `python -m paper_2507_16676_amd.build` "
             "(hipcc, gfx950). There is no CPU fallback.")
+    # torch first: it brings its own HIP runtime, and the library must bind to
+    # that same runtime (the one that owns torch's memory and streams); loaded
+    # before torch, it would pull in the system runtime instead and launches
+    # on torch's streams fail
+    import torch  # noqa: F401
     L = ctypes.CDLL(LIB_PATH)
     L.fabft_attn_fwd.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f]
     L.fabft_attn_fwd.restype = _i
     L.fabft_attn_fwd_nocheck.argtypes = [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f]
     L.fabft_attn_fwd_nocheck.restype = _i
     L.fabft_attn_fwd_inject.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
-                                        _f, ctypes.POINTER(FabftFault), _vp, _vp]
+                                        _f, ctypes.POINTER(FabftFault), _vp, _vp, _vp, _vp]
     L.fabft_attn_fwd_inject.restype = _i
     L.fabft_set_stream.argtypes = [_vp]
     L.fabft_set_stream.restype = None
@@ -64,6 +69,10 @@ def _load() -> ctypes.CDLL:
     L.fabft_set_threshold.restype = _i
     L.fabft_get_threshold.argtypes = [_fp, _fp]
     L.fabft_get_threshold.restype = None
+    L.fabft_set_weighted_check.argtypes = [_i]
+    L.fabft_set_weighted_check.restype = None
+    L.fabft_get_weighted_check.argtypes = []
+    L.fabft_get_weighted_check.restype = _i
     L.fabft_key_tile.argtypes = [_i]
     L.fabft_key_tile.restype = _i
     L.fabft_query_tile.argtypes = []
@@ -76,6 +85,7 @@ def _load() -> ctypes.CDLL:
 
 EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
+           "fabft_set_weighted_check", "fabft_get_weighted_check",
            "fabft_key_tile", "fabft_query_tile", "fabft_status_str")
 
 
@@ -107,6 +117,15 @@ def get_threshold() -> tuple[float, float]:
     a, b = ctypes.c_float(), ctypes.c_float()
     _load().fabft_get_threshold(ctypes.byref(a), ctypes.byref(b))
     return a.value, b.value
+
+
+def set_weighted_check(on: bool):
+    """Switch the second, weighted checksum on or off (process-global)."""
+    _load().fabft_set_weighted_check(int(bool(on)))
+
+
+def get_weighted_check() -> bool:
+    return bool(_load().fabft_get_weighted_check())
 
 
 def key_tile(d: int) -> int:
@@ -187,8 +206,9 @@ class Fault:
 
 
 def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
-                    fault: Fault | None = None, out=None):
-    """Debug / fault-injection forward. Returns (o, resid, flags, pred, actual)."""
+                    fault: Fault | None = None, out=None, weighted_out: bool = False):
+    """Debug / fault-injection forward. Returns (o, resid, flags, pred, actual),
+    followed by (pred_w, actual_w) with weighted_out=True."""
     import torch
     B, H, Lq, Lk, d = _shape(q, k, v)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
@@ -200,18 +220,27 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
         pred = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
         actual = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
     else:
-        o, resid, flags, pred, actual = out
+        o, resid, flags, pred, actual = out[:5]
+    pw = aw = None
+    if weighted_out:
+        pw = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+        aw = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
     f = fault.to_c() if fault is not None else None
     _stream(dev)
     _check(_load().fabft_attn_fwd_inject(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                                       resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
                                       int(bool(causal)), scale,
                                       ctypes.byref(f) if f is not None else None,
-                                      pred.data_ptr(), actual.data_ptr()),
+                                      pred.data_ptr(), actual.data_ptr(),
+                                      pw.data_ptr() if pw is not None else None,
+                                      aw.data_ptr() if aw is not None else None),
            "fabft_attn_fwd_inject")
+    if weighted_out:
+        return o, resid, flags, pred, actual, pw, aw
     return o, resid, flags, pred, actual
 
 
 __all__ = ["attn_fwd", "attn_fwd_inject", "Fault", "FabftError", "set_threshold",
-           "get_threshold", "key_tile", "query_tile", "status_str", "lib", "LIB_PATH",
-           "EXPORTS", "FLAG_RESID", "FLAG_NONFINITE"]
+           "get_threshold", "set_weighted_check", "get_weighted_check", "key_tile",
+           "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "FLAG_RESID",
+           "FLAG_NONFINITE", "FLAG_WEIGHTED"]

@@ -227,9 +227,12 @@ def summarize(path):
 
 def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000):
     """Fault-free runs on seeds seed0..seed0+seeds-1: count flagged rows
-    (must be 0) and track rho = max |resid| / (sum_j |O_ij| + |pred|)."""
+    (must be 0) and track rho = max |resid| / (sum_j |O_ij| + |pred|), and
+    with the weighted check on, the same ratio for it (rho_w)."""
     torch = _torch()
-    from . import attn_fwd, attn_fwd_inject, get_threshold
+    from . import attn_fwd, attn_fwd_inject, get_threshold, get_weighted_check
+    weighted = get_weighted_check()
+    rho_w_max = 0.0
     o = resid = flags = None
     flagged_total = 0
     flagged_seeds = []
@@ -244,10 +247,15 @@ def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000):
             flagged_total += nf
             flagged_seeds.append(s)
         if rho_every and i % rho_every == 0:
-            od, rd, fd, pred, actual = attn_fwd_inject(q, k, v, causal=w.causal, scale=w.scale)
-            M = od.float().abs().sum(dim=-1) + pred.abs()
+            od, rd, fd, pred, actual, pw, aw = attn_fwd_inject(
+                q, k, v, causal=w.causal, scale=w.scale, weighted_out=True)
+            absO = od.float().abs().sum(dim=-1)
+            M = absO + pred.abs()
             ratio = (rd.abs() / M.clamp_min(1e-30)).max().item()
             rho_max = max(rho_max, ratio)
+            if weighted:
+                Mw = absO + pw.abs()
+                rho_w_max = max(rho_w_max, ((pw - aw).abs() / Mw.clamp_min(1e-30)).max().item())
             rho_seeds += 1
         if log_every and (i + 1) % log_every == 0:
             print(f"[sweep] {i + 1} seeds, flagged rows {flagged_total}, rho max {rho_max:.3e}, "
@@ -256,7 +264,9 @@ def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000):
     res = {"workload": w.name, "seeds": seeds, "seed0": seed0, "rows_checked": rows,
            "flagged_rows": flagged_total, "flagged_seeds": flagged_seeds[:100],
            "rho_max": rho_max, "rho_seeds": rho_seeds, "threshold": get_threshold(),
-           "seconds": time.time() - t0}
+           "weighted_check": weighted, "seconds": time.time() - t0}
+    if weighted:
+        res["rho_w_max"] = rho_w_max
     if out_path:
         with open(out_path, "w") as f:
             json.dump(res, f, indent=1)
@@ -275,16 +285,24 @@ def main(argv=None):
     c.add_argument("--seed", type=int, default=0)
     c.add_argument("--out", required=True)
     c.add_argument("--summary")
+    c.add_argument("--weighted", action="store_true",
+                   help="also run the weighted (alternating-sign) checksum")
     s = sub.add_parser("sweep")
     s.add_argument("--workload", default="dec_l4096")
     s.add_argument("--seeds", type=int, default=10000)
     s.add_argument("--seed0", type=int, default=1)
     s.add_argument("--rho-every", type=int, default=100)
     s.add_argument("--out", required=True)
+    s.add_argument("--weighted", action="store_true",
+                   help="also run the weighted (alternating-sign) checksum")
     a = ap.parse_args(argv)
     w = W.WORKLOADS[a.workload]
+    if a.weighted:
+        from . import set_weighted_check
+        set_weighted_check(True)
     if a.cmd == "campaign":
         summ = run_campaign(w, a.runs, a.out, seed=a.seed, start=a.start)
+        summ["weighted_check"] = bool(a.weighted)
         txt = json.dumps(summ, indent=1)
         if a.summary:
             with open(a.summary, "w") as f:

@@ -21,6 +21,9 @@ hipStream_t g_stream = nullptr;
 // output at d = 128.
 float g_tau_rel = 1.0f / 65536.0f;
 float g_tau_abs = 0.0f;
+// Weighted second checksum (weights (-1)^j) next to the paper's one; off by
+// default, so that the default path is the paper's single check.
+int g_wcheck = 0;
 
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -54,6 +57,9 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.flags = flags;
   p.pred = nullptr;
   p.actual = nullptr;
+  p.pred_w = nullptr;
+  p.actual_w = nullptr;
+  p.wcheck = g_wcheck;
   p.Lq = Lq;
   p.Lk = Lk;
   p.n_qt = n_qt;
@@ -96,7 +102,8 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
 
 int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,
                           uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
-                          float scale, const fabft_fault* f, float* pred, float* actual) {
+                          float scale, const fabft_fault* f, float* pred, float* actual,
+                          float* pred_w, float* actual_w) {
   int n_qt = 0, grid = 0;
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
@@ -104,6 +111,8 @@ int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, 
   fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid);
   p.pred = pred;
   p.actual = actual;
+  p.pred_w = pred_w;
+  p.actual_w = actual_w;
   if (f && f->site != FABFT_SITE_NONE) {
     if (f->b < 0 || f->b >= B || f->h < 0 || f->h >= H) return FABFT_E_FAULT;
     const int off = Lk - Lq;
@@ -154,6 +163,10 @@ void fabft_get_threshold(float* tau_rel, float* tau_abs) {
   if (tau_rel) *tau_rel = g_tau_rel;
   if (tau_abs) *tau_abs = g_tau_abs;
 }
+
+void fabft_set_weighted_check(int on) { g_wcheck = on ? 1 : 0; }
+
+int fabft_get_weighted_check(void) { return g_wcheck; }
 
 int fabft_key_tile(int d) {
   if (d != 64 && d != 128) return FABFT_E_HEADDIM;

@@ -18,6 +18,9 @@ struct FwdParams {
   uint8_t* flags;
   float* pred;    // injection/debug kernels only; may be null
   float* actual;  // injection/debug kernels only; may be null
+  float* pred_w;    // weighted check, debug kernels only; may be null
+  float* actual_w;  // weighted check, debug kernels only; may be null
+  int wcheck;     // 1: also run the weighted (alternating-sign) checksum
   int Lq, Lk;
   int n_qt;       // query tiles per head
   int grid;       // workgroups = B * H * n_qt

@@ -71,6 +71,7 @@ constexpr int kStages = 4;               // LDS ring depth (tiles in flight + 1)
 constexpr int kBc = 64;                  // keys per tile
 constexpr float kLazy = 8.0f;            // max drift (exp2 domain) before a rescale
 constexpr uint32_t kOnes = 0x3f803f80u;  // bf16 pair (1.0, 1.0)
+constexpr uint32_t kAlt = 0xbf803f80u;   // bf16 pair (1.0, -1.0): weights (-1)^j
 
 __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(
@@ -115,6 +116,19 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2));
 }
 
+// The bits of x, opaque to the optimiser. This file is built with relaxed
+// NaN rules, under which the compiler may fold an exponent-bits test of a
+// float into "is infinite" and drop the NaN case; the asm keeps the test on
+// the actual bits.
+__device__ __forceinline__ uint32_t opaque_bits(float x) {
+  uint32_t b = __float_as_uint(x);
+  asm volatile("" : "+v"(b));
+  return b;
+}
+__device__ __forceinline__ bool nonfinite_bits(float x) {
+  return (opaque_bits(x) & 0x7f800000u) == 0x7f800000u;
+}
+
 // Row r of an MFMA 32-row block reads key 16*(r>>4) + 8*((r>>2)&1) + 4*((r>>3)&1) + (r&3)
 __device__ __forceinline__ int swap_bits23(int r) {
   return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1);
@@ -152,14 +166,18 @@ struct Tile {
 };
 
 // Rows of the small A operand that yields c and l: sumrow(V) as bf16 hi and
-// lo parts, ones, zeros (MFMA rows >= 3 read the zero row).
-enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3 };
+// lo parts, ones, zeros, and the weighted row sums sum_j (-1)^j V_kj as hi
+// and lo parts. MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9
+// read WHi, WLo (accumulator elements 4, 5 of lanes 0-31); the others read
+// the zero row.
+enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRowWLo = 5,
+       kVsmRows = 6 };
 
 template <int D>
 struct Stage {
   uint16_t k[kBc * D];
   uint16_t v[kBc * D];
-  uint16_t vsm[4][kBc];
+  uint16_t vsm[kVsmRows][kBc];
 };
 
 template <int D, bool CAUSAL, bool CHECK, bool INJECT>
@@ -241,8 +259,13 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     const int st_i = tid >> 7, row = kRowOnes + ((tid >> 6) & 1), key = tid & 63;
     stage[st_i].vsm[row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
   }
-  // MFMA row of this lane in the c / l operand (rows 0, 1 only with the checksum)
-  const int vsm_row = (mrow < 2 && !CHECK) ? kRowZero : min(mrow, (int)kRowZero);
+  // row of the c / l operand that MFMA row mrow reads (rows 0, 1, 8, 9 only
+  // with the checksum)
+  const int vsm_row = mrow == 2                ? (int)kRowOnes
+                      : (!CHECK)               ? (int)kRowZero
+                      : mrow < 2               ? mrow
+                      : (mrow == 8 || mrow == 9) ? (int)kRowWHi + (mrow - 8)
+                                               : (int)kRowZero;
 
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
   // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk repeat
@@ -272,7 +295,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     Stage<D>& st = stage[buf];
     const int key = tid >> 3, part = tid & 7;
     constexpr int CPT = CPR / 8;   // chunks per thread
-    float a = 0.f;
+    float a = 0.f, aw = 0.f;
     u32x4 ch[CPT];
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
@@ -281,12 +304,26 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       for (int e = 0; e < 4; ++e) a = dot2(ch[i][e], kOnes, a);
     }
     const float vs = group8_sum(a);
+    // the chunk's columns start at an even j, so the pair weights are (1, -1)
+    float vw = 0.f;
+    if (p.wcheck) {
+#pragma unroll
+      for (int i = 0; i < CPT; ++i)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) aw = dot2(ch[i][e], kAlt, aw);
+      vw = group8_sum(aw);
+    }
     if (part == 0) {
       const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
       const float hif = __uint_as_float(hi << 16);
       const uint32_t lo = pack_bf16x2(vs - hif, 0.f) & 0xffffu;
       st.vsm[kRowVsHi][key] = (uint16_t)hi;
       st.vsm[kRowVsLo][key] = (uint16_t)lo;
+      const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
+      const float whif = __uint_as_float(whi << 16);
+      const uint32_t wlo = pack_bf16x2(vw - whif, 0.f) & 0xffffu;
+      st.vsm[kRowWHi][key] = (uint16_t)whi;
+      st.vsm[kRowWLo][key] = (uint16_t)wlo;
     }
     if constexpr (INJECT) {
       // V site: flip a bit of V[key][col] of this workgroup's copy after
@@ -524,7 +561,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
   const float l_tot = sum_xor32(aux[2]);
   const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-  float act = 0.f, absum = 0.f;
+  float act = 0.f, absum = 0.f, act_w = 0.f;
 #pragma unroll
   for (int db = 0; db < NDB; ++db)
 #pragma unroll
@@ -533,6 +570,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       oacc[db][i] = x;
       act += x;
       absum += __builtin_fabsf(x);
+      // column 32db + 8(i/4) + 4grp + i%4 is even iff i is even
+      act_w += (i & 1) ? -x : x;
     }
   if (qrow < Lq) {
     uint16_t* orow = p.o + qbase + (size_t)qrow * D;
@@ -554,8 +593,19 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     const float M = absum + __builtin_fabsf(pred);
     // non-finite test on the bits (this file is built with relaxed NaN rules);
     // a non-finite residual also fails the threshold comparison
-    const bool nonfinite = (__float_as_uint(r) & 0x7f800000u) == 0x7f800000u;
-    const uint8_t f = nonfinite ? 3 : (__builtin_fabsf(r) <= p.tau_rel * M + p.tau_abs ? 0 : 1);
+    bool nonfinite = nonfinite_bits(r);
+    uint8_t f = (__builtin_fabsf(r) <= p.tau_rel * M + p.tau_abs) ? 0 : 1;
+    // weighted check: pred_w = c_w / l against sum_j (-1)^j O_ij (the same
+    // threshold rule; |w_j| = 1 keeps M)
+    float pred_w = 0.f;
+    if (p.wcheck) {
+      act_w = sum_xor32(act_w);
+      pred_w = sum_xor32(aux[4] + aux[5]) * inv;
+      const float rw = pred_w - act_w;
+      nonfinite = nonfinite || nonfinite_bits(rw);
+      if (!(__builtin_fabsf(rw) <= p.tau_rel * (absum + __builtin_fabsf(pred_w)) + p.tau_abs)) f |= 4;
+    }
+    if (nonfinite) f |= 3;
     if (grp == 0 && qrow < Lq) {
       const size_t ri = (size_t)bh * Lq + qrow;
       p.resid[ri] = r;
@@ -563,6 +613,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       if constexpr (INJECT) {
         if (p.pred) p.pred[ri] = pred;
         if (p.actual) p.actual[ri] = act;
+        if (p.pred_w) p.pred_w[ri] = pred_w;
+        if (p.actual_w) p.actual_w[ri] = p.wcheck ? act_w : 0.f;
       }
     }
   }
@@ -570,6 +622,9 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 
 template <int D, bool CAUSAL, bool CHECK, bool INJECT>
 static int launch_t(const FwdParams& p, hipStream_t stream) {
+  // the thread's last-error slot may hold an error of an unrelated earlier
+  // HIP call (made by the caller); clear it so that only this launch counts
+  (void)hipGetLastError();
   hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT>), dim3(p.grid), dim3(kThreads), 0,
                      stream, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;

@@ -104,12 +104,12 @@ def test_nocheck_rejects_bad_arguments():
 def test_inject_rejects_bad_faults(fault):
     f = fault.to_c()
     rc = F.lib().fabft_attn_fwd_inject(P, P, P, P, P, P, 1, 2, 8, 8, 128, 1, 0.1,
-                                       ctypes.byref(f), None, None)
+                                       ctypes.byref(f), None, None, None, None)
     assert rc == F.E_FAULT
 
 
 def test_inject_rejects_unknown_site():
     f = F.FabftFault(9, 0, 0, 0, 0, 0, 0)
     rc = F.lib().fabft_attn_fwd_inject(P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 0.1,
-                                       ctypes.byref(f), None, None)
+                                       ctypes.byref(f), None, None, None, None)
     assert rc == F.E_FAULT

@@ -368,3 +368,89 @@ def test_threshold_flags_rule():
     assert f.tolist() == [0, 0, 1, 3, 3, 0]
     f = oracle.threshold_flags(resid, Oabs, pred, tau_rel=0.0, tau_abs=0.0)
     assert f.tolist() == [0, 1, 1, 3, 3, 1]
+
+
+# --------------------------------------------------------------------------
+# the weighted checksum (an extension next to the paper's check)
+# --------------------------------------------------------------------------
+
+def _brute_weighted(q, k, v, causal, scale, w):
+    """Pure-Python loops: pred_w and actual_w row by row."""
+    Lq, Lk, d = len(q), len(k), len(v[0])
+    out = []
+    for i in range(Lq):
+        keys = [j for j in range(Lk) if not causal or j <= i + (Lk - Lq)]
+        if not keys:
+            out.append((0.0, 0.0))
+            continue
+        s = {j: scale * sum(q[i][t] * k[j][t] for t in range(len(q[0]))) for j in keys}
+        mx = max(s.values())
+        e = {j: math.exp(s[j] - mx) for j in keys}
+        l = sum(e.values())
+        pw = sum(e[j] * sum(w[c] * v[j][c] for c in range(d)) for j in keys) / l
+        aw = sum(w[c] * sum(e[j] * v[j][c] for j in keys) / l for c in range(d))
+        out.append((pw, aw))
+    return np.array(out)
+
+
+@pytest.mark.parametrize("causal", [False, True])
+@pytest.mark.parametrize("Lq,Lk,d", [(1, 1, 2), (3, 5, 4), (5, 3, 3), (6, 6, 5)])
+def test_weighted_brute_force(causal, Lq, Lk, d):
+    seed = 7 * Lq + 3 * Lk + d + (1 if causal else 0)
+    q, k, v = _rand((Lq, d), seed), _rand((Lk, d), seed + 1), _rand((Lk, d), seed + 2)
+    w = [1.0 if j % 2 == 0 else -1.0 for j in range(d)]
+    ref = _brute_weighted(q.tolist(), k.tolist(), v.tolist(), causal, 0.6, w)
+    r = oracle.weighted_check_head(q, k, v, causal, 0.6)
+    assert np.allclose(r["pred_w"], ref[:, 0], rtol=0, atol=1e-13)
+    assert np.allclose(r["actual_w"], ref[:, 1], rtol=0, atol=1e-13)
+
+
+def test_weighted_with_unit_weights_is_the_paper_check():
+    q, k, v = _rand((17, 8), 31), _rand((23, 8), 32), _rand((23, 8), 33)
+    r1 = oracle.weighted_check_head(q, k, v, True, 0.4, w=np.ones(8))
+    r0 = oracle.attention_head(q, k, v, True, 0.4)
+    assert np.allclose(r1["pred_w"], r0["pred"], rtol=0, atol=1e-14)
+    assert np.allclose(r1["actual_w"], r0["actual"], rtol=0, atol=1e-14)
+
+
+def test_weighted_identity_values_closed_form():
+    # V = I: pred_w_i = sum_k softmax(s_i)_k w_k (scipy's softmax)
+    Lq, Lk = 7, 10
+    q, k = _rand((Lq, 4), 41), _rand((Lk, 4), 42)
+    r = oracle.weighted_check_head(q, k, np.eye(Lk), False, 1.1)
+    sm = scipy.special.softmax(1.1 * (q @ k.T), axis=1)
+    w = np.where(np.arange(Lk) % 2 == 0, 1.0, -1.0)
+    assert np.allclose(r["pred_w"], sm @ w, rtol=0, atol=1e-15)
+    assert np.allclose(r["actual_w"], sm @ w, rtol=0, atol=1e-15)
+
+
+def test_weighted_rows_along_the_weights():
+    # V_kj = a_k w_j: both sides are d * (softmax-weighted mean of a)
+    Lq, Lk, d = 5, 9, 6
+    q, k = _rand((Lq, 3), 51), _rand((Lk, 3), 52)
+    a = _rand((Lk,), 53)
+    w = oracle.alternating_weights(d)
+    v = a[:, None] * w[None, :]
+    r = oracle.weighted_check_head(q, k, v, True, 0.8)
+    s = 0.8 * (q @ k.T)
+    s = np.where(oracle.visible_mask(Lq, Lk, True), s, -np.inf)
+    sm = scipy.special.softmax(s, axis=1)
+    assert np.allclose(r["pred_w"], d * (sm @ a), rtol=0, atol=1e-13)
+    assert np.allclose(r["actual_w"], d * (sm @ a), rtol=0, atol=1e-13)
+
+
+def test_weighted_sees_a_zero_sum_value_row():
+    # a planted change of p~ at a key whose V row sums to 0 is invisible to
+    # the paper's check but moves the weighted one (the reason for it)
+    d = 8
+    v = _rand((4, d), 61)
+    v[2] = np.repeat(_rand((d // 2,), 62), 2) * np.tile([1.0, -1.0], d // 2)
+    assert abs(v[2].sum()) < 1e-12
+    w = oracle.alternating_weights(d)
+    p = np.array([0.3, 0.2, 0.4, 0.1])
+    dp = np.zeros(4)
+    dp[2] = 0.05
+    # sums of the output row before and after the change, divided by l
+    plain = ((p + dp) @ v).sum() - (p @ v).sum()
+    weighted = ((p + dp) @ v) @ w - (p @ v) @ w
+    assert abs(plain) < 1e-12 and abs(weighted) > 1e-3
