@@ -180,7 +180,8 @@ struct Stage {
   uint16_t vsm[kVsmRows][kBc];
 };
 
-template <int D, bool CAUSAL, bool CHECK, bool INJECT>
+// WCHK: the weighted second checksum is compiled in (only with CHECK)
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK>
 __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   constexpr int BC = kBc;
   constexpr int CPR = Tile<D>::CPR;
@@ -259,12 +260,12 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     const int st_i = tid >> 7, row = kRowOnes + ((tid >> 6) & 1), key = tid & 63;
     stage[st_i].vsm[row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
   }
-  // row of the c / l operand that MFMA row mrow reads (rows 0, 1, 8, 9 only
-  // with the checksum)
+  // row of the c / l operand that MFMA row mrow reads (rows 0, 1 only with
+  // the checksum, rows 8, 9 only with the weighted one)
   const int vsm_row = mrow == 2                ? (int)kRowOnes
                       : (!CHECK)               ? (int)kRowZero
                       : mrow < 2               ? mrow
-                      : (mrow == 8 || mrow == 9) ? (int)kRowWHi + (mrow - 8)
+                      : (WCHK && (mrow == 8 || mrow == 9)) ? (int)kRowWHi + (mrow - 8)
                                                : (int)kRowZero;
 
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
@@ -306,7 +307,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     const float vs = group8_sum(a);
     // the chunk's columns start at an even j, so the pair weights are (1, -1)
     float vw = 0.f;
-    if (p.wcheck) {
+    if constexpr (WCHK) {
 #pragma unroll
       for (int i = 0; i < CPT; ++i)
 #pragma unroll
@@ -319,11 +320,13 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       const uint32_t lo = pack_bf16x2(vs - hif, 0.f) & 0xffffu;
       st.vsm[kRowVsHi][key] = (uint16_t)hi;
       st.vsm[kRowVsLo][key] = (uint16_t)lo;
-      const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
-      const float whif = __uint_as_float(whi << 16);
-      const uint32_t wlo = pack_bf16x2(vw - whif, 0.f) & 0xffffu;
-      st.vsm[kRowWHi][key] = (uint16_t)whi;
-      st.vsm[kRowWLo][key] = (uint16_t)wlo;
+      if constexpr (WCHK) {
+        const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
+        const float whif = __uint_as_float(whi << 16);
+        const uint32_t wlo = pack_bf16x2(vw - whif, 0.f) & 0xffffu;
+        st.vsm[kRowWHi][key] = (uint16_t)whi;
+        st.vsm[kRowWLo][key] = (uint16_t)wlo;
+      }
     }
     if constexpr (INJECT) {
       // V site: flip a bit of V[key][col] of this workgroup's copy after
@@ -598,7 +601,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     // weighted check: pred_w = c_w / l against sum_j (-1)^j O_ij (the same
     // threshold rule; |w_j| = 1 keeps M)
     float pred_w = 0.f;
-    if (p.wcheck) {
+    if constexpr (WCHK) {
       act_w = sum_xor32(act_w);
       pred_w = sum_xor32(aux[4] + aux[5]) * inv;
       const float rw = pred_w - act_w;
@@ -614,33 +617,37 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
         if (p.pred) p.pred[ri] = pred;
         if (p.actual) p.actual[ri] = act;
         if (p.pred_w) p.pred_w[ri] = pred_w;
-        if (p.actual_w) p.actual_w[ri] = p.wcheck ? act_w : 0.f;
+        if (p.actual_w) p.actual_w[ri] = WCHK ? act_w : 0.f;
       }
     }
   }
 }
 
-template <int D, bool CAUSAL, bool CHECK, bool INJECT>
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK>
 static int launch_t(const FwdParams& p, hipStream_t stream) {
   // the thread's last-error slot may hold an error of an unrelated earlier
   // HIP call (made by the caller); clear it so that only this launch counts
   (void)hipGetLastError();
-  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT>), dim3(p.grid), dim3(kThreads), 0,
-                     stream, p);
+  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK>), dim3(p.grid), dim3(kThreads),
+                     0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+template <int D, bool CAUSAL>
+static int launch_c(const FwdParams& p, int mode, hipStream_t s) {
+  // mode 0: no checksum, 1: checksum, 2: checksum + injection/debug
+  if (mode == 0) return launch_t<D, CAUSAL, false, false, false>(p, s);
+  if (mode == 1) {
+    if (p.wcheck) return launch_t<D, CAUSAL, true, false, true>(p, s);
+    return launch_t<D, CAUSAL, true, false, false>(p, s);
+  }
+  if (p.wcheck) return launch_t<D, CAUSAL, true, true, true>(p, s);
+  return launch_t<D, CAUSAL, true, true, false>(p, s);
 }
 
 template <int D>
 static int launch_d(const FwdParams& p, bool causal, int mode, hipStream_t s) {
-  // mode 0: no checksum, 1: checksum, 2: checksum + injection/debug
-  if (causal) {
-    if (mode == 0) return launch_t<D, true, false, false>(p, s);
-    if (mode == 1) return launch_t<D, true, true, false>(p, s);
-    return launch_t<D, true, true, true>(p, s);
-  }
-  if (mode == 0) return launch_t<D, false, false, false>(p, s);
-  if (mode == 1) return launch_t<D, false, true, false>(p, s);
-  return launch_t<D, false, true, true>(p, s);
+  return causal ? launch_c<D, true>(p, mode, s) : launch_c<D, false>(p, mode, s);
 }
 
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream) {
