@@ -97,6 +97,22 @@ int fabft_set_threshold(float tau_rel, float tau_abs);
 void fabft_get_threshold(float* tau_rel, float* tau_abs);
 
 /*
+ * Global check per head (Algorithm 3, the check summed over all queries of
+ * the attention; the paper's single check, Eq. 5 in the per-query form of
+ * Eq. 6-7): from the O and resid that fabft_attn_fwd wrote, for every
+ * (b, h): gsum = sum_i resid_i = sum_i pred_i - sum_i actual_i and
+ * A = sum_i sum_j |O_ij| (bf16 O), both accumulated in fp64 in a fixed order,
+ * and gflags = FABFT_FLAG_RESID if NOT |gsum| <= tau_rel * A + tau_abs
+ * (FABFT_FLAG_NONFINITE | FABFT_FLAG_RESID if gsum is not finite), with the
+ * current threshold. o: bf16 [B, H, Lq, d] (16-byte aligned), resid: fp32
+ * [B, H, Lq], gsum: fp64 [B, H], gflags: uint8 [B, H]; device pointers.
+ * A fault must move its row's sum by about Lq times more than the per-row
+ * check needs to be seen here. Asynchronous on the library stream.
+ */
+int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq,
+                       int d, double* gsum, uint8_t* gflags);
+
+/*
  * Second, weighted checksum (an extension beyond the paper, which uses one
  * checksum per row): with on != 0, every checksum-on launch also carries
  *   c_w <- c_w * exp(m_old - m_new) + (sum_j (-1)^j V_kj) * p~_k
@@ -126,10 +142,18 @@ enum {
                           before the P V product */
   FABFT_SITE_O = 3,    /* fp32 output accumulator o_ij right after the
                           P V product of key tile `tile` */
-  FABFT_SITE_V = 4     /* bf16 V_kj in the on-chip copy of one workgroup,
+  FABFT_SITE_V = 4,    /* bf16 V_kj in the on-chip copy of one workgroup,
                           after sumrow_k(V) was taken, before the P V product
                           reads it; every query row of that workgroup that
                           sees key k reads the flipped value */
+  /* checker state (Section IV-B counts faults there as possible false
+     positives): */
+  FABFT_SITE_C = 5,    /* fp32 checksum accumulator c of query row `row`
+                          (its high part) after the update of key tile `tile` */
+  FABFT_SITE_L = 6,    /* fp32 accumulator l of the row after key tile `tile` */
+  FABFT_SITE_M = 7     /* fp32 running max (scale * log2 e units) of the row,
+                          as held by the lane of the row's first key half,
+                          after the exponentials of key tile `tile` */
 };
 
 /*
@@ -139,7 +163,8 @@ enum {
  * a tile that row i processes: t*key_tile <= last visible key of i). For V:
  * row = key k, col = column j, tile = query tile (rows tile*query_tile ..
  * tile*query_tile + query_tile - 1) whose workgroup holds the flipped copy.
- * bit: 0..31 for fp32 sites (S, O), 0..15 for bf16 sites (P, V).
+ * For C, L, M: row = query i, col = 0, tile as for O.
+ * bit: 0..31 for fp32 sites (S, O, C, L, M), 0..15 for bf16 sites (P, V).
  */
 typedef struct {
   int site, b, h, row, col, tile, bit;

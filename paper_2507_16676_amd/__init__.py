@@ -29,8 +29,9 @@ FABFT_OK = 0
 E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD = \
     -1, -2, -3, -4, -5, -6, -7, -8
 FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED = 1, 2, 4
-SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V = 0, 1, 2, 3, 4
-SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V}
+SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M = 0, 1, 2, 3, 4, 5, 6, 7
+SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V,
+         "C": SITE_C, "L": SITE_L, "M": SITE_M}
 
 
 class FabftFault(ctypes.Structure):
@@ -69,6 +70,8 @@ def _load() -> ctypes.CDLL:
     L.fabft_set_threshold.restype = _i
     L.fabft_get_threshold.argtypes = [_fp, _fp]
     L.fabft_get_threshold.restype = None
+    L.fabft_global_check.argtypes = [_vp, _vp, _i, _i, _i, _i, _vp, _vp]
+    L.fabft_global_check.restype = _i
     L.fabft_set_weighted_check.argtypes = [_i]
     L.fabft_set_weighted_check.restype = None
     L.fabft_get_weighted_check.argtypes = []
@@ -85,7 +88,7 @@ def _load() -> ctypes.CDLL:
 
 EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
-           "fabft_set_weighted_check", "fabft_get_weighted_check",
+           "fabft_global_check", "fabft_set_weighted_check", "fabft_get_weighted_check",
            "fabft_key_tile", "fabft_query_tile", "fabft_status_str")
 
 
@@ -189,10 +192,27 @@ def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, check: b
     return o, resid, flags
 
 
+def global_check(o, resid):
+    """Per-head global check from attn_fwd's o and resid: returns (gsum [B, H]
+    fp64 = sum of the row residuals, gflags [B, H] uint8)."""
+    import torch
+    if o.dtype != torch.bfloat16 or not o.is_cuda or not o.is_contiguous() or o.dim() != 4:
+        raise ValueError("o must be a contiguous bf16 [B, H, Lq, d] GPU tensor")
+    B, H, Lq, d = o.shape
+    if tuple(resid.shape) != (B, H, Lq) or resid.dtype != torch.float32 or not resid.is_contiguous():
+        raise ValueError("resid must be a contiguous fp32 [B, H, Lq] tensor")
+    gsum = torch.empty((B, H), dtype=torch.float64, device=o.device)
+    gflags = torch.empty((B, H), dtype=torch.uint8, device=o.device)
+    _stream(o.device)
+    _check(_load().fabft_global_check(o.data_ptr(), resid.data_ptr(), B, H, Lq, d,
+                                      gsum.data_ptr(), gflags.data_ptr()), "fabft_global_check")
+    return gsum, gflags
+
+
 @dataclass
 class Fault:
     """One single-bit fault for attn_fwd_inject (fields as in fabft_fault)."""
-    site: str          # "S", "P", "O", "V" or "none"
+    site: str          # "S", "P", "O", "V", "C", "L", "M" or "none"
     b: int = 0
     h: int = 0
     row: int = 0
@@ -240,7 +260,7 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
     return o, resid, flags, pred, actual
 
 
-__all__ = ["attn_fwd", "attn_fwd_inject", "Fault", "FabftError", "set_threshold",
+__all__ = ["attn_fwd", "attn_fwd_inject", "global_check", "Fault", "FabftError", "set_threshold",
            "get_threshold", "set_weighted_check", "get_weighted_check", "key_tile",
            "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "FLAG_RESID",
            "FLAG_NONFINITE", "FLAG_WEIGHTED"]

@@ -40,8 +40,11 @@ import time
 import numpy as np
 
 SITES = ("S", "P", "O", "V")
-SITE_BITS = {"S": 32, "P": 16, "O": 32, "V": 16}
-EXP_BITS = {"S": range(23, 31), "P": range(7, 15), "O": range(23, 31), "V": range(7, 15)}
+# checker state (c, l, running max): the paper's false-positive sources
+CHECKER_SITES = ("C", "L", "M")
+SITE_BITS = {"S": 32, "P": 16, "O": 32, "V": 16, "C": 32, "L": 32, "M": 32}
+EXP_BITS = {"S": range(23, 31), "P": range(7, 15), "O": range(23, 31), "V": range(7, 15),
+            "C": range(23, 31), "L": range(23, 31), "M": range(23, 31)}
 SIG_REL = 2.0 ** -8
 
 
@@ -85,14 +88,14 @@ def draw_fault(run: int, w, key_tile: int, query_tile: int, sites=SITES):
     h = int(rng.integers(w.H))
     off = w.Lk - w.Lq
     bit = int(rng.integers(SITE_BITS[site]))
-    if site in ("S", "P", "O"):
+    if site in ("S", "P", "O", "C", "L", "M"):
         while True:
             row = int(rng.integers(w.Lq))
             last = min(w.Lk - 1, row + off) if w.causal else w.Lk - 1
             if last >= 0:
                 break
-        if site == "O":
-            col = int(rng.integers(w.d))
+        if site in ("O", "C", "L", "M"):
+            col = int(rng.integers(w.d)) if site == "O" else 0
             tile = int(rng.integers(last // key_tile + 1))
         else:
             col = int(rng.integers(last + 1))
@@ -143,7 +146,7 @@ def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES
     appending one JSON line per run to out_path; runs already in the file
     are skipped."""
     torch = _torch()
-    from . import attn_fwd_inject, key_tile, query_tile
+    from . import attn_fwd_inject, global_check, key_tile, query_tile
     done = set()
     if os.path.exists(out_path):
         with open(out_path) as f:
@@ -173,9 +176,12 @@ def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES
             o, resid, flags, pred, actual = attn_fwd_inject(qh, kh, vh, causal=w.causal,
                                                             scale=w.scale, fault=f_local)
             res = classify(o[0, 0], gold[(b, h)][0, 0], flags[0, 0])
+            # the paper's single check per attention, on the same output
+            _, gflag = global_check(o, resid)
             rec = {"run": r, "site": f.site, "b": b, "h": h, "row": f.row, "col": f.col,
                    "tile": f.tile, "bit": f.bit,
-                   "exponent_bit": f.bit in EXP_BITS[f.site], **res}
+                   "exponent_bit": f.bit in EXP_BITS[f.site], **res,
+                   "global_flag": int(gflag[0, 0])}
             out.write(json.dumps(rec) + "\n")
             n_new += 1
             if log_every and n_new % log_every == 0:
@@ -209,8 +215,17 @@ def summarize(path):
                 head[r["outcome"]] += 1
     n = head["detected"] + head["silent"]
     rate = head["detected"] / n if n else float("nan")
+    # the same significant runs judged by the global per-head check alone
+    gl = {"detected": 0, "silent": 0}
+    for r in recs:
+        if (r["site"] in ("P", "O", "V") and r["exponent_bit"] and "global_flag" in r
+                and r["outcome"] in ("detected", "silent")):
+            gl["detected" if r["global_flag"] else "silent"] += 1
+    ng = gl["detected"] + gl["silent"]
     per_site = {}
-    for s in SITES:
+    for s in SITES + CHECKER_SITES:
+        if ("all", s) not in table:
+            continue
         t = table.get(("all", s), {})
         tot = sum(t.values())
         per_site[s] = {**t, "runs": tot,
@@ -221,6 +236,13 @@ def summarize(path):
             "headline": {"what": "exponent-bit flips at P, O, V: detected / (detected + silent)",
                          "detected": head["detected"], "silent": head["silent"],
                          "rate": rate, "wilson95": wilson(head["detected"], n)},
+            "headline_global": {"what": "the same significant runs, flagged by the per-head "
+                                        "global check (Alg. 3 single check)",
+                                "detected": gl["detected"], "silent": gl["silent"],
+                                "rate": gl["detected"] / ng if ng else float("nan"),
+                                "wilson95": wilson(gl["detected"], ng)},
+            "global_false_alarms": sum(1 for r in recs if r.get("global_flag")
+                                       and r["outcome"] in ("false_positive", "benign")),
             "false_positives": sum(1 for r in recs if r["outcome"] == "false_positive"),
             "per_site": per_site, "per_bit": per_bit}
 
@@ -287,6 +309,8 @@ def main(argv=None):
     c.add_argument("--summary")
     c.add_argument("--weighted", action="store_true",
                    help="also run the weighted (alternating-sign) checksum")
+    c.add_argument("--sites", default="S,P,O,V",
+                   help="comma-separated fault sites to draw from (S,P,O,V,C,L,M)")
     s = sub.add_parser("sweep")
     s.add_argument("--workload", default="dec_l4096")
     s.add_argument("--seeds", type=int, default=10000)
@@ -301,7 +325,8 @@ def main(argv=None):
         from . import set_weighted_check
         set_weighted_check(True)
     if a.cmd == "campaign":
-        summ = run_campaign(w, a.runs, a.out, seed=a.seed, start=a.start)
+        summ = run_campaign(w, a.runs, a.out, seed=a.seed, start=a.start,
+                            sites=tuple(a.sites.split(",")))
         summ["weighted_check"] = bool(a.weighted)
         txt = json.dumps(summ, indent=1)
         if a.summary:

@@ -124,8 +124,12 @@ int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, 
         if (causal && f->col > f->row + off) return FABFT_E_FAULT;
         if (f->bit < 0 || f->bit >= (f->site == FABFT_SITE_S ? 32 : 16)) return FABFT_E_FAULT;
         break;
+      case FABFT_SITE_C:
+      case FABFT_SITE_L:
+      case FABFT_SITE_M:
       case FABFT_SITE_O: {
-        if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= d) return FABFT_E_FAULT;
+        const int ncol = f->site == FABFT_SITE_O ? d : 1;
+        if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= ncol) return FABFT_E_FAULT;
         if (f->bit < 0 || f->bit >= 32) return FABFT_E_FAULT;
         const long long last = causal ? std::min<long long>(Lk - 1, (long long)f->row + off)
                                       : (long long)Lk - 1;
@@ -162,6 +166,18 @@ int fabft_set_threshold(float tau_rel, float tau_abs) {
 void fabft_get_threshold(float* tau_rel, float* tau_abs) {
   if (tau_rel) *tau_rel = g_tau_rel;
   if (tau_abs) *tau_abs = g_tau_abs;
+}
+
+int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq, int d,
+                       double* gsum, uint8_t* gflags) {
+  if (!o || !resid || !gsum || !gflags) return FABFT_E_NULL;
+  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  if (B < 1 || H < 1 || Lq < 1) return FABFT_E_SHAPE;
+  if (static_cast<long long>(B) * H > INT_MAX) return FABFT_E_SHAPE;
+  if (!aligned16(o)) return FABFT_E_ALIGN;
+  const int rc = fabft::launch_global(static_cast<const uint16_t*>(o), resid, B * H, Lq, d,
+                                      g_tau_rel, g_tau_abs, gsum, gflags, g_stream);
+  return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
 }
 
 void fabft_set_weighted_check(int on) { g_wcheck = on ? 1 : 0; }

@@ -32,6 +32,8 @@ struct FwdParams {
 // mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream);
 int key_tile(int d);
+int launch_global(const uint16_t* o, const float* resid, int BH, int Lq, int d, float tau_rel,
+                  float tau_abs, double* gsum, uint8_t* gflag, hipStream_t stream);
 
 }  // namespace fabft
 

@@ -443,6 +443,12 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           pb[kb][h][e] = pack_bf16x2(sacc[kb][8 * h + 2 * e], sacc[kb][8 * h + 2 * e + 1]);
+    if constexpr (INJECT) {
+      // M site (checker state): the running max of the lane holding the
+      // row's first key half, after this tile's exponentials
+      if (p.f_site == 7 && bh == p.f_bh && qrow == p.f_row && t == p.f_tile && grp == 0)
+        m2_run = __uint_as_float(__float_as_uint(m2_run) ^ (1u << p.f_bit));
+    }
 
     // c = c*alpha + sumrow(V) p~ and l = l*alpha + sum p~ (Alg. 3): the
     // c / l MFMA reads p~ before the P site and the P V product
@@ -461,6 +467,17 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
         const u32x4 a = *reinterpret_cast<const u32x4*>(&st.vsm[vsm_row][32 * kb + 16 * h + 8 * grp]);
         aux = mfma32(a, pb[kb][h], aux);
       }
+    if constexpr (INJECT) {
+      // C and L sites (checker state): the fp32 accumulator c (its high
+      // part) or l of the row after this tile's update
+      if ((p.f_site == 5 || p.f_site == 6) && bh == p.f_bh && qrow == p.f_row &&
+          t == p.f_tile && grp == 0) {
+        const int el = p.f_site == 5 ? 0 : 2;
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          if (i == el) aux[i] = __uint_as_float(__float_as_uint(aux[i]) ^ (1u << p.f_bit));
+      }
+    }
     if constexpr (INJECT) {
       if (p.f_site == 2 && bh == p.f_bh && qrow == p.f_row) {
         const int kl = p.f_col - kv0;
@@ -656,5 +673,61 @@ int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t str
 }
 
 int key_tile(int d) { return (d == 64 || d == 128) ? kBc : 0; }
+
+// ---- global check of one head (Alg. 3, the check accumulated over all
+// queries; Eq. 5 in its per-query form, Eq. 6-7): R = sum_i (pred_i -
+// actual_i) = sum_i resid_i and A = sum_i sum_j |O_ij|, in fp64, one
+// workgroup per (b, h), with a fixed reduction order (deterministic).
+constexpr int kGThreads = 256;
+
+__global__ __launch_bounds__(kGThreads) void global_check_kernel(
+    const uint16_t* __restrict__ o, const float* __restrict__ resid, int Lq, int d,
+    float tau_rel, float tau_abs, double* __restrict__ gsum, uint8_t* __restrict__ gflag) {
+  __shared__ double red_r[kGThreads];
+  __shared__ double red_a[kGThreads];
+  const int bh = blockIdx.x;
+  const int tid = threadIdx.x;
+  const float* r = resid + (size_t)bh * Lq;
+  const uint16_t* ob = o + (size_t)bh * Lq * d;
+  double sr = 0.0, sa = 0.0;
+  for (int i = tid; i < Lq; i += kGThreads) sr += (double)r[i];
+  // O as 8-element chunks (rows are 16-byte aligned: d is 64 or 128)
+  const size_t nchunk = (size_t)Lq * d / 8;
+  for (size_t c = tid; c < nchunk; c += kGThreads) {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(ob + 8 * c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      sa += (double)__builtin_fabsf(__uint_as_float(w[e] << 16));
+      sa += (double)__builtin_fabsf(__uint_as_float(w[e] & 0xffff0000u));
+    }
+  }
+  red_r[tid] = sr;
+  red_a[tid] = sa;
+  __syncthreads();
+  for (int s = kGThreads / 2; s > 0; s >>= 1) {
+    if (tid < s) {
+      red_r[tid] += red_r[tid + s];
+      red_a[tid] += red_a[tid + s];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const double R = red_r[0], A = red_a[0];
+    const uint64_t bits = __double_as_longlong(R);
+    const bool nonfinite = ((bits >> 52) & 0x7ff) == 0x7ff;
+    uint8_t f = (__builtin_fabs(R) <= (double)tau_rel * A + (double)tau_abs) ? 0 : 1;
+    if (nonfinite) f = 3;
+    gsum[bh] = R;
+    gflag[bh] = f;
+  }
+}
+
+int launch_global(const uint16_t* o, const float* resid, int BH, int Lq, int d, float tau_rel,
+                  float tau_abs, double* gsum, uint8_t* gflag, hipStream_t stream) {
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(global_check_kernel, dim3(BH), dim3(kGThreads), 0, stream, o, resid, Lq, d,
+                     tau_rel, tau_abs, gsum, gflag);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
 
 }  // namespace fabft

@@ -100,6 +100,10 @@ def test_nocheck_rejects_bad_arguments():
     F.Fault("V", row=8, col=0, tile=0),           # key >= Lk
     F.Fault("V", row=0, col=0, tile=1),           # only one query tile
     F.Fault("V", row=0, col=0, tile=0, bit=16),
+    F.Fault("C", row=0, col=1, tile=0),           # checker sites have one column
+    F.Fault("L", row=8, col=0, tile=0),           # row >= Lq
+    F.Fault("M", row=3, col=0, tile=1),           # tile past the row's keys
+    F.Fault("C", row=0, col=0, tile=0, bit=32),
 ])
 def test_inject_rejects_bad_faults(fault):
     f = fault.to_c()
@@ -113,3 +117,13 @@ def test_inject_rejects_unknown_site():
     rc = F.lib().fabft_attn_fwd_inject(P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 0.1,
                                        ctypes.byref(f), None, None, None, None)
     assert rc == F.E_FAULT
+
+
+def test_global_check_validation():
+    L = F.lib()
+    assert L.fabft_global_check(None, P, 1, 1, 8, 128, P, P) == F.E_NULL
+    assert L.fabft_global_check(P, P, 1, 1, 8, 128, None, P) == F.E_NULL
+    assert L.fabft_global_check(P, P, 1, 1, 8, 96, P, P) == F.E_HEADDIM
+    assert L.fabft_global_check(P, P, 0, 1, 8, 128, P, P) == F.E_SHAPE
+    assert L.fabft_global_check(P, P, 1, 1, 0, 128, P, P) == F.E_SHAPE
+    assert L.fabft_global_check(P + 2, P, 1, 1, 8, 128, P, P) == F.E_ALIGN

@@ -20,8 +20,9 @@ def _valid(f, w, bc, qt):
         assert 0 <= f.row < w.Lq and 0 <= f.col < w.Lk
         assert not w.causal or f.col <= f.row + off
         assert 0 <= f.bit < (32 if f.site == "S" else 16)
-    elif f.site == "O":
-        assert 0 <= f.row < w.Lq and 0 <= f.col < w.d and 0 <= f.bit < 32
+    elif f.site in ("O", "C", "L", "M"):
+        ncol = w.d if f.site == "O" else 1
+        assert 0 <= f.row < w.Lq and 0 <= f.col < ncol and 0 <= f.bit < 32
         last = min(w.Lk - 1, f.row + off) if w.causal else w.Lk - 1
         assert 0 <= f.tile * bc <= last
     else:
@@ -45,6 +46,17 @@ def test_draws_are_valid_and_cover_sites_and_bits(w):
     assert {s for s, _ in seen} == set(C.SITES)
     for s in C.SITES:
         assert {b for site, b in seen if site == s} == set(range(C.SITE_BITS[s]))
+
+
+@pytest.mark.parametrize("w", [W_C, W.Workload("rect", 2, 3, 300, 77, 64, True, 0.125)])
+def test_checker_site_draws_are_valid(w):
+    bc, qt = 64, 256
+    seen = set()
+    for r in range(1500):
+        f = C.draw_fault(r, w, bc, qt, sites=C.CHECKER_SITES)
+        _valid(f, w, bc, qt)
+        seen.add(f.site)
+    assert seen == set(C.CHECKER_SITES)
 
 
 def test_draws_are_reproducible():

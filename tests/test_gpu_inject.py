@@ -104,3 +104,37 @@ def test_s_site_flip_is_consistent(golden):
     others = flags.clone()
     others[0, 0, 120] = 0
     assert int(others.sum()) == 0
+
+
+# --------------------------------------------------------------------------
+# checker-state sites: c, l and the running max
+# --------------------------------------------------------------------------
+
+def test_c_site_flip_is_a_false_alarm(golden):
+    # the checksum accumulator is only read by the check: O is unchanged
+    f = F.Fault("C", b=0, h=1, row=210, col=0, tile=1, bit=30)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    (_, (o0, r0, f0, p0, a0)) = golden
+    assert torch.equal(o.view(torch.int16), o0.view(torch.int16))
+    assert torch.equal(actual, a0)
+    assert int(flags[0, 1, 210]) != 0
+    assert int(flags.sum()) == int(flags[0, 1, 210])
+
+
+def test_l_site_flip_moves_o_and_pred_together(golden):
+    # l divides both o and c: the ratio the check tests is unchanged
+    f = F.Fault("L", b=0, h=0, row=150, col=0, tile=1, bit=26)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    (_, (o0, r0, f0, p0, a0)) = golden
+    assert _changed_rows(o, o0) == {(0, 0, 150)}
+    assert int(flags.sum()) == 0
+
+
+def test_m_site_flip_stays_in_its_row(golden):
+    f = F.Fault("M", b=0, h=1, row=290, col=0, tile=2, bit=28)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    (_, (o0, r0, f0, p0, a0)) = golden
+    assert _changed_rows(o, o0) <= {(0, 1, 290)}
+    others = flags.clone()
+    others[0, 1, 290] = 0
+    assert int(others.sum()) == 0
