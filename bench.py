@@ -79,6 +79,42 @@ def time_launches(fn, steps, stream):
     return evs[0].elapsed_time(evs[-1]), per
 
 
+DECODE_SHAPES = [(4, 32, 1, 32768), (4, 32, 16, 32768), (1, 32, 1, 131072), (8, 8, 64, 8192)]
+
+
+def decode_sweep(d: int = 128, splits=(0, 4, 8, 16, 32, 64), reps: int = 20):
+    """K/V bytes streamed per second for the one-pass forward (nsplit 0) and
+    the key-split forward on decode shapes, checksum on, non-causal."""
+    import torch
+    import paper_2507_16676_amd as F
+    import workloads as W
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream(dev)
+    for (B, H, Lq, Lk) in DECODE_SHAPES:
+        w = W.Workload(f"decode_b{B}_h{H}_q{Lq}_k{Lk}", B, H, Lq, Lk, d, False, d ** -0.5)
+        q, k, v = make_device_inputs(w, dev)
+        kv_bytes = 2 * B * H * Lk * d * 2
+        rows = {}
+        for ns in splits:
+            if ns == 0:
+                fn = lambda: F.attn_fwd(q, k, v, causal=False, scale=w.scale)
+            else:
+                ws = torch.empty(F.splitkv_workspace_bytes(B, H, Lq, d, ns), dtype=torch.uint8,
+                                 device=dev)
+                fn = (lambda ns=ns, ws=ws: F.attn_fwd_splitkv(q, k, v, causal=False, scale=w.scale,
+                                                             nsplit=ns, workspace=ws))
+            for _ in range(5):
+                fn()
+            t, _ = time_launches(fn, reps, stream)
+            us = 1e3 * t / reps
+            rows[f"nsplit_{ns}" if ns else "one_pass"] = {"us": round(us, 1),
+                                                          "TB/s": round(kv_bytes / us / 1e6, 3)}
+        print(json.dumps({"workload": w.name, "kv_bytes": kv_bytes,
+                          "default_nsplit": F.splitkv_default_splits(B, H, Lq, Lk, d),
+                          "results": rows}), flush=True)
+
+
 def cpu_baseline(w, target_s: float):
     """Time the fp64 oracle on the host for a bounded sample of the workload:
     whole heads (all query rows) of batch entry 0, drawn with the same
@@ -121,6 +157,9 @@ def main():
     ap.add_argument("--rounds", type=int, default=5,
                     help="interleaved on/off rounds for the overhead figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-sweep", action="store_true",
+                    help="instead of the benchmark line: time the one-pass and the key-split "
+                         "forward on decode shapes (few queries, many keys), one JSON line each")
     ap.add_argument("--weighted", action="store_true",
                     help="also run the weighted second checksum (an extension)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -138,6 +177,9 @@ def main():
     import torch
     import paper_2507_16676_amd as F
     F.set_weighted_check(args.weighted)
+    if args.decode_sweep:
+        decode_sweep()
+        return
     import workloads as W
 
     w = W.WORKLOADS[args.workload]

@@ -52,7 +52,8 @@ enum {
   FABFT_E_LAUNCH = -5,   /* the kernel launch failed */
   FABFT_E_SCALE = -6,    /* scale negative, NaN or infinite */
   FABFT_E_FAULT = -7,    /* fault descriptor out of range */
-  FABFT_E_THRESHOLD = -8 /* threshold negative or NaN */
+  FABFT_E_THRESHOLD = -8, /* threshold negative or NaN */
+  FABFT_E_WORKSPACE = -9  /* workspace smaller than fabft_splitkv_workspace_bytes */
 };
 
 /* Detection flags, one byte per query row. */
@@ -84,6 +85,34 @@ int fabft_attn_fwd(const void* q, const void* k, const void* v, void* o,
 int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v,
                            void* o, int B, int H, int Lq, int Lk, int d,
                            int causal, float scale);
+
+/*
+ * Bytes of workspace that fabft_attn_fwd_splitkv needs: one partial-state
+ * record of (d + 4) floats per (b, h, query row, split). Negative status for
+ * d not 64/128, a size < 1 or nsplit outside 1..64.
+ */
+long long fabft_splitkv_workspace_bytes(int B, int H, int Lq, int d, int nsplit);
+
+/*
+ * fabft_attn_fwd with the keys split into nsplit ranges of whole key tiles
+ * (for few queries over many keys, e.g. decode): each workgroup runs
+ * Algorithm 3 on one range and writes the partial state of every row
+ * (running max m, l, c and the unnormalised o[d]) to the caller's workspace;
+ * a merge kernel then combines the ranges with m = max_s m_s and
+ * x = sum_s x_s exp(m_s - m) for x in {l, o, c} -- c merges exactly like one
+ * more column of o (Eq. 10) -- and applies the per-row check after the
+ * merge, so faults in the merge of o are covered too. O, resid and flags
+ * have the same meaning and layout as in fabft_attn_fwd; results match it to
+ * rounding (not bitwise). workspace: device memory of at least
+ * fabft_splitkv_workspace_bytes(B, H, Lq, d, nsplit) bytes, 16-byte aligned,
+ * owned by the caller, overwritten. nsplit: 1..64. Asynchronous (two
+ * launches in order on the library stream).
+ */
+int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v,
+                           void* o, float* resid, uint8_t* flags,
+                           int B, int H, int Lq, int Lk, int d, int causal,
+                           float scale, int nsplit, void* workspace,
+                           long long workspace_bytes);
 
 /* Stream for all subsequent launches (a hipStream_t; NULL = null stream). */
 void fabft_set_stream(void* hip_stream);

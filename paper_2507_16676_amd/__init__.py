@@ -26,8 +26,8 @@ _vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
 _fp = ctypes.POINTER(ctypes.c_float)
 
 FABFT_OK = 0
-E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD = \
-    -1, -2, -3, -4, -5, -6, -7, -8
+E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE = \
+    -1, -2, -3, -4, -5, -6, -7, -8, -9
 FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED = 1, 2, 4
 SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M = 0, 1, 2, 3, 4, 5, 6, 7
 SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V,
@@ -70,6 +70,11 @@ def _load() -> ctypes.CDLL:
     L.fabft_set_threshold.restype = _i
     L.fabft_get_threshold.argtypes = [_fp, _fp]
     L.fabft_get_threshold.restype = None
+    L.fabft_splitkv_workspace_bytes.argtypes = [_i, _i, _i, _i, _i]
+    L.fabft_splitkv_workspace_bytes.restype = ctypes.c_longlong
+    L.fabft_attn_fwd_splitkv.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                         _f, _i, _vp, ctypes.c_longlong]
+    L.fabft_attn_fwd_splitkv.restype = _i
     L.fabft_global_check.argtypes = [_vp, _vp, _i, _i, _i, _i, _vp, _vp]
     L.fabft_global_check.restype = _i
     L.fabft_set_weighted_check.argtypes = [_i]
@@ -87,6 +92,7 @@ def _load() -> ctypes.CDLL:
 
 
 EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
+           "fabft_attn_fwd_splitkv", "fabft_splitkv_workspace_bytes",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
            "fabft_global_check", "fabft_set_weighted_check", "fabft_get_weighted_check",
            "fabft_key_tile", "fabft_query_tile", "fabft_status_str")
@@ -192,6 +198,51 @@ def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, check: b
     return o, resid, flags
 
 
+def splitkv_workspace_bytes(B: int, H: int, Lq: int, d: int, nsplit: int) -> int:
+    r = _load().fabft_splitkv_workspace_bytes(int(B), int(H), int(Lq), int(d), int(nsplit))
+    _check(min(int(r), 0), "fabft_splitkv_workspace_bytes")
+    return int(r)
+
+
+def splitkv_default_splits(B: int, H: int, Lq: int, Lk: int, d: int) -> int:
+    """A split count that gives the launch about 512 workgroups (two per CU),
+    with at least 8 key tiles per split and at most 64 splits (measured on
+    decode shapes: one to 64 queries over 8K-128K keys)."""
+    n_qt = -(-Lq // query_tile())
+    tiles = -(-Lk // key_tile(d))
+    return max(1, min(64, -(-512 // (B * H * n_qt)), tiles // 8))
+
+
+def attn_fwd_splitkv(q, k, v, causal: bool = False, scale: float | None = None,
+                     nsplit: int | None = None, workspace=None, out=None):
+    """Flash-ABFT forward with the keys split into nsplit ranges and a merge
+    (for few queries over many keys). Returns (o, resid, flags). nsplit
+    defaults to splitkv_default_splits(...). workspace: optional uint8 GPU
+    tensor of at least splitkv_workspace_bytes(...) bytes."""
+    import torch
+    B, H, Lq, Lk, d = _shape(q, k, v)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dev = q.device
+    if nsplit is None:
+        nsplit = splitkv_default_splits(B, H, Lq, Lk, d)
+    need = splitkv_workspace_bytes(B, H, Lq, d, nsplit)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    if out is not None:
+        o, resid, flags = out
+    else:
+        o = torch.empty_like(q)
+        resid = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+        flags = torch.empty((B, H, Lq), dtype=torch.uint8, device=dev)
+    _stream(dev)
+    _check(_load().fabft_attn_fwd_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                          resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
+                                          int(bool(causal)), scale, int(nsplit),
+                                          workspace.data_ptr(), workspace.numel()),
+           "fabft_attn_fwd_splitkv")
+    return o, resid, flags
+
+
 def global_check(o, resid):
     """Per-head global check from attn_fwd's o and resid: returns (gsum [B, H]
     fp64 = sum of the row residuals, gflags [B, H] uint8)."""
@@ -260,7 +311,9 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
     return o, resid, flags, pred, actual
 
 
-__all__ = ["attn_fwd", "attn_fwd_inject", "global_check", "Fault", "FabftError", "set_threshold",
+__all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_splitkv", "splitkv_workspace_bytes",
+           "splitkv_default_splits",
+           "global_check", "Fault", "FabftError", "set_threshold",
            "get_threshold", "set_weighted_check", "get_weighted_check", "key_tile",
            "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "FLAG_RESID",
            "FLAG_NONFINITE", "FLAG_WEIGHTED"]

@@ -26,6 +26,7 @@ float g_tau_abs = 0.0f;
 int g_wcheck = 0;
 
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kMaxSplits = 64;   // the merge reads one split per lane
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -60,6 +61,9 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.pred_w = nullptr;
   p.actual_w = nullptr;
   p.wcheck = g_wcheck;
+  p.nsplit = 1;
+  p.split_tiles = 0;
+  p.ws = nullptr;
   p.Lq = Lq;
   p.Lk = Lk;
   p.n_qt = n_qt;
@@ -168,6 +172,40 @@ void fabft_get_threshold(float* tau_rel, float* tau_abs) {
   if (tau_abs) *tau_abs = g_tau_abs;
 }
 
+long long fabft_splitkv_workspace_bytes(int B, int H, int Lq, int d, int nsplit) {
+  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  if (B < 1 || H < 1 || Lq < 1 || nsplit < 1 || nsplit > kMaxSplits) return FABFT_E_SHAPE;
+  return static_cast<long long>(B) * H * Lq * nsplit * fabft::split_record_floats(d) *
+         static_cast<long long>(sizeof(float));
+}
+
+int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v, void* o, float* resid,
+                           uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                           float scale, int nsplit, void* workspace, long long workspace_bytes) {
+  int n_qt = 0, grid = 0;
+  int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
+  if (rc != FABFT_OK) return rc;
+  if (!resid || !flags || !workspace) return FABFT_E_NULL;
+  if (nsplit < 1 || nsplit > kMaxSplits) return FABFT_E_SHAPE;
+  if (!aligned16(workspace)) return FABFT_E_ALIGN;
+  const long long need = fabft_splitkv_workspace_bytes(B, H, Lq, d, nsplit);
+  if (need < 0) return static_cast<int>(need);
+  if (workspace_bytes < need) return FABFT_E_WORKSPACE;
+  const long long g = static_cast<long long>(grid) * nsplit;
+  if (g > INT_MAX) return FABFT_E_SHAPE;
+  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid);
+  const int bc = fabft::key_tile(d);
+  const int tiles = (Lk + bc - 1) / bc;
+  p.nsplit = nsplit;
+  p.split_tiles = (tiles + nsplit - 1) / nsplit;
+  p.ws = static_cast<float*>(workspace);
+  p.grid = static_cast<int>(g);
+  rc = fabft::launch_fwd(p, d, causal != 0, 3, g_stream);
+  if (rc != 0) return FABFT_E_LAUNCH;
+  rc = fabft::launch_merge(p, d, B * H, g_stream);
+  return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
+}
+
 int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq, int d,
                        double* gsum, uint8_t* gflags) {
   if (!o || !resid || !gsum || !gflags) return FABFT_E_NULL;
@@ -202,6 +240,7 @@ const char* fabft_status_str(int status) {
     case FABFT_E_SCALE: return "scale must be finite and >= 0";
     case FABFT_E_FAULT: return "fault descriptor out of range";
     case FABFT_E_THRESHOLD: return "threshold must be >= 0";
+    case FABFT_E_WORKSPACE: return "workspace too small (see fabft_splitkv_workspace_bytes)";
     default: return "unknown status";
   }
 }

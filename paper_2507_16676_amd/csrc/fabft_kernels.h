@@ -21,6 +21,12 @@ struct FwdParams {
   float* pred_w;    // weighted check, debug kernels only; may be null
   float* actual_w;  // weighted check, debug kernels only; may be null
   int wcheck;     // 1: also run the weighted (alternating-sign) checksum
+  // split over the keys (mode 3): workgroup (head, query tile, split) runs
+  // key tiles [split*split_tiles, (split+1)*split_tiles) and writes the
+  // partial state of each row to ws (see launch_merge)
+  int nsplit;
+  int split_tiles;
+  float* ws;
   int Lq, Lk;
   int n_qt;       // query tiles per head
   int grid;       // workgroups = B * H * n_qt
@@ -29,9 +35,16 @@ struct FwdParams {
   int f_site, f_bh, f_row, f_col, f_tile, f_bit;  // fault (site 0 = none)
 };
 
-// mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection
+// mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection,
+// 3: checksum on, one key split per workgroup (partial states to p.ws)
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream);
 int key_tile(int d);
+// Partial-state record of (head, row, split) in the split workspace, in
+// floats: m (exp2 domain), l, c, c_w, then the d unnormalised outputs o.
+inline int split_record_floats(int d) { return d + 4; }
+// Merge the partial states of every row (mode 3 writes them) into O, resid
+// and flags.
+int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream);
 int launch_global(const uint16_t* o, const float* resid, int BH, int Lq, int d, float tau_rel,
                   float tau_abs, double* gsum, uint8_t* gflag, hipStream_t stream);
 

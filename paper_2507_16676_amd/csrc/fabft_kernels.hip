@@ -49,6 +49,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <climits>
+
 #include "fabft_kernels.h"
 
 namespace fabft {
@@ -57,6 +59,7 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -180,8 +183,9 @@ struct Stage {
   uint16_t vsm[kVsmRows][kBc];
 };
 
-// WCHK: the weighted second checksum is compiled in (only with CHECK)
-template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK>
+// WCHK: the weighted second checksum is compiled in (only with CHECK).
+// SPLIT: the workgroup runs one key split and writes partial row states.
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT>
 __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   constexpr int BC = kBc;
   constexpr int CPR = Tile<D>::CPR;
@@ -208,8 +212,14 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   // head count divisible by 8 a head still stays on one XCD.
   const int G = p.grid;
   const int bid = blockIdx.x;
-  int bh, qt;
-  if (CAUSAL) {
+  int bh, qt, split = 0;
+  if (SPLIT) {
+    // the splits of one (head, query tile) are neighbours
+    split = bid % p.nsplit;
+    const int lg = bid / p.nsplit;
+    bh = lg / p.n_qt;
+    qt = lg - bh * p.n_qt;
+  } else if (CAUSAL) {
     const int BH = G / p.n_qt;
     const int qr = bid / BH;
     bh = bid - qr * BH;
@@ -234,6 +244,12 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   if (CAUSAL) kend = min(Lk, q0 + kBr + off);
   // wave-uniform (the division runs on the vector ALU): scalar branches
   const int ntiles = __builtin_amdgcn_readfirstlane(kend > 0 ? (kend + BC - 1) / BC : 0);
+  // key tiles [t_lo, t_end) of this workgroup
+  int t_lo = 0, t_end = ntiles;
+  if (SPLIT) {
+    t_lo = min(ntiles, split * p.split_tiles);
+    t_end = min(ntiles, t_lo + p.split_tiles);
+  }
 
   const int wq_lo = q0 + 32 * wave;  // first query row of this wave
   const int qrow = wq_lo + mrow;
@@ -274,7 +290,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   const uint16_t* kg = p.k + kbase;
   const uint16_t* vg = p.v + kbase;
   auto issue = [&](int t) {
-    if (t >= ntiles) return;
+    if (t >= t_end) return;
     Stage<D>& st = stage[t % kStages];
     const int kv0 = t * BC;
 #pragma unroll
@@ -548,34 +564,56 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 
   // ---- pipeline: tiles t+1 and t+2 in flight while tile t is processed
   constexpr int LPT = 2 * NLD;   // loads per thread per tile (K and V)
-  if (ntiles > 0) {
-    issue(0);
-    issue(1);
-    issue(2);
-    // tile 0 complete; tiles 1 and 2 may be outstanding
-    if (ntiles >= 3) wait_vmcnt<2 * LPT>();
-    else if (ntiles == 2) wait_vmcnt<LPT>();
+  if (t_end > t_lo) {
+    issue(t_lo);
+    issue(t_lo + 1);
+    issue(t_lo + 2);
+    // first tile complete; the next two may be outstanding
+    if (t_end - t_lo >= 3) wait_vmcnt<2 * LPT>();
+    else if (t_end - t_lo == 2) wait_vmcnt<LPT>();
     else wait_vmcnt<0>();
     __syncthreads();
-    if constexpr (CHECK) sumrow(0, 0);
+    if constexpr (CHECK) sumrow(t_lo % kStages, t_lo);
   }
   // A use of Q here, on every path into the loop, puts the compiler's own
   // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
   // also waits for tiles 1 and 2) before the loop rather than inside it.
 #pragma unroll
   for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
-  for (int t = 0; t < ntiles; ++t) {
+  for (int t = t_lo; t < t_end; ++t) {
     // tile t+1 complete (tile t+2 may still be in flight); after the barrier
     // every wave is done with tile t-1, whose stage takes tile t+3
-    if (t + 2 < ntiles) wait_vmcnt<LPT>();
+    if (t + 2 < t_end) wait_vmcnt<LPT>();
     else wait_vmcnt<0>();
     __syncthreads();
-    if (!CAUSAL || t * BC <= wq_lo + 31 + off) compute(t);
+    // waves whose rows see none of this tile's keys, or that hold no row
+    // below Lq, skip it (they still load and take sumrow for the others)
+    if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(t);
     issue(t + 3);
     if constexpr (CHECK) {
-      if (t + 1 < ntiles) sumrow((t + 1) % kStages, t + 1);
+      if (t + 1 < t_end) sumrow((t + 1) % kStages, t + 1);
     }
 
+  }
+
+  if constexpr (SPLIT) {
+    // ---- partial state of each row for this key split (merged by
+    // merge_kernel): m, l, c, c_w and the unnormalised o, in the same
+    // exponent reference m (exp2 domain)
+    const float l_p = sum_xor32(aux[2]);
+    const float c_p = sum_xor32(aux[0] + aux[1]);
+    const float cw_p = WCHK ? sum_xor32(aux[4] + aux[5]) : 0.f;
+    if (qrow < Lq) {
+      float* rec = p.ws + (((size_t)bh * Lq + qrow) * p.nsplit + split) * (D + 4);
+      if (grp == 0) *reinterpret_cast<f32x4*>(rec) = f32x4{m2_run, l_p, c_p, cw_p};
+#pragma unroll
+      for (int db = 0; db < NDB; ++db)
+#pragma unroll
+        for (int a = 0; a < 4; ++a)
+          *reinterpret_cast<f32x4*>(rec + 4 + 32 * db + 8 * a + 4 * grp) =
+              f32x4{oacc[db][4 * a], oacc[db][4 * a + 1], oacc[db][4 * a + 2], oacc[db][4 * a + 3]};
+    }
+    return;
   }
 
   // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
@@ -640,31 +678,128 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   }
 }
 
-template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK>
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT>
 static int launch_t(const FwdParams& p, hipStream_t stream) {
   // the thread's last-error slot may hold an error of an unrelated earlier
   // HIP call (made by the caller); clear it so that only this launch counts
   (void)hipGetLastError();
-  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK>), dim3(p.grid), dim3(kThreads),
-                     0, stream, p);
+  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK, SPLIT>), dim3(p.grid),
+                     dim3(kThreads), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 template <int D, bool CAUSAL>
 static int launch_c(const FwdParams& p, int mode, hipStream_t s) {
-  // mode 0: no checksum, 1: checksum, 2: checksum + injection/debug
-  if (mode == 0) return launch_t<D, CAUSAL, false, false, false>(p, s);
+  // mode 0: no checksum, 1: checksum, 2: checksum + injection/debug,
+  // 3: checksum, key split
+  if (mode == 0) return launch_t<D, CAUSAL, false, false, false, false>(p, s);
   if (mode == 1) {
-    if (p.wcheck) return launch_t<D, CAUSAL, true, false, true>(p, s);
-    return launch_t<D, CAUSAL, true, false, false>(p, s);
+    if (p.wcheck) return launch_t<D, CAUSAL, true, false, true, false>(p, s);
+    return launch_t<D, CAUSAL, true, false, false, false>(p, s);
   }
-  if (p.wcheck) return launch_t<D, CAUSAL, true, true, true>(p, s);
-  return launch_t<D, CAUSAL, true, true, false>(p, s);
+  if (mode == 3) {
+    if (p.wcheck) return launch_t<D, CAUSAL, true, false, true, true>(p, s);
+    return launch_t<D, CAUSAL, true, false, false, true>(p, s);
+  }
+  if (p.wcheck) return launch_t<D, CAUSAL, true, true, true, false>(p, s);
+  return launch_t<D, CAUSAL, true, true, false, false>(p, s);
 }
 
 template <int D>
 static int launch_d(const FwdParams& p, bool causal, int mode, hipStream_t s) {
   return causal ? launch_c<D, true>(p, mode, s) : launch_c<D, false>(p, mode, s);
+}
+
+// ---- merge of the key splits: one wave per query row. With m = max_s m_s
+// and w_s = 2^(m_s - m): l = sum_s w_s l_s, o = sum_s w_s o_s, and c (and
+// c_w) merge exactly like one more column of o (Eq. 10); then O = o / l,
+// pred = c / l, actual = sum_j O_ij and the row's check as in the main
+// kernel. Splits that saw no key have m_s = -inf and weight 0.
+constexpr int kMergeWaves = 4;
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x = __builtin_fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+template <int D, bool WCHK>
+__global__ __launch_bounds__(64 * kMergeWaves) void merge_kernel(FwdParams p, int rows_per_head) {
+  constexpr int R = D + 4;
+  constexpr int CPL = D / 64;   // output columns per lane
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int nrb = (rows_per_head + kMergeWaves - 1) / kMergeWaves;
+  const int bh = blockIdx.x / nrb;
+  const int row = (blockIdx.x - bh * nrb) * kMergeWaves + wave;
+  if (row >= rows_per_head) return;   // wave-uniform; no barriers below
+  const int ns = p.nsplit;
+  const float* rec = p.ws + ((size_t)bh * rows_per_head + row) * ns * R;
+  const float ms = lane < ns ? rec[(size_t)lane * R] : -__builtin_inff();
+  const float m = wave_max(ms);
+  const float w = (ms == -__builtin_inff()) ? 0.f : __builtin_amdgcn_exp2f(ms - m);
+  const float l = wave_sum(lane < ns ? w * rec[(size_t)lane * R + 1] : 0.f);
+  const float c = wave_sum(lane < ns ? w * rec[(size_t)lane * R + 2] : 0.f);
+  const float cw = WCHK ? wave_sum(lane < ns ? w * rec[(size_t)lane * R + 3] : 0.f) : 0.f;
+  float o[CPL];
+#pragma unroll
+  for (int u = 0; u < CPL; ++u) o[u] = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const float ws_ = __shfl(w, s);
+#pragma unroll
+    for (int u = 0; u < CPL; ++u) o[u] = __builtin_fmaf(ws_, rec[(size_t)s * R + 4 + lane + 64 * u], o[u]);
+  }
+  const float inv = l > 0.f ? 1.0f / l : 0.f;
+  float act = 0.f, absum = 0.f, act_w = 0.f;
+  uint16_t* orow = p.o + ((size_t)bh * rows_per_head + row) * D;
+#pragma unroll
+  for (int u = 0; u < CPL; ++u) {
+    const float x = o[u] * inv;
+    act += x;
+    absum += __builtin_fabsf(x);
+    act_w += (lane & 1) ? -x : x;   // column lane + 64u has the parity of lane
+    orow[lane + 64 * u] = (uint16_t)(pack_bf16x2(x, 0.f) & 0xffffu);
+  }
+  act = wave_sum(act);
+  absum = wave_sum(absum);
+  const float pred = c * inv;
+  const float r = pred - act;
+  bool nonfinite = nonfinite_bits(r);
+  uint8_t f = (__builtin_fabsf(r) <= p.tau_rel * (absum + __builtin_fabsf(pred)) + p.tau_abs) ? 0 : 1;
+  if constexpr (WCHK) {
+    act_w = wave_sum(act_w);
+    const float pred_w = cw * inv;
+    const float rw = pred_w - act_w;
+    nonfinite = nonfinite || nonfinite_bits(rw);
+    if (!(__builtin_fabsf(rw) <= p.tau_rel * (absum + __builtin_fabsf(pred_w)) + p.tau_abs)) f |= 4;
+  }
+  if (nonfinite) f |= 3;
+  if (lane == 0) {
+    const size_t ri = (size_t)bh * rows_per_head + row;
+    p.resid[ri] = r;
+    p.flags[ri] = f;
+  }
+}
+
+int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream) {
+  const int nrb = (p.Lq + kMergeWaves - 1) / kMergeWaves;
+  const long long g = (long long)nheads * nrb;
+  if (g > INT_MAX) return -1;
+  (void)hipGetLastError();
+  const dim3 grid((unsigned)g), block(64 * kMergeWaves);
+  if (d == 128) {
+    if (p.wcheck) hipLaunchKernelGGL((merge_kernel<128, true>), grid, block, 0, stream, p, p.Lq);
+    else hipLaunchKernelGGL((merge_kernel<128, false>), grid, block, 0, stream, p, p.Lq);
+  } else {
+    if (p.wcheck) hipLaunchKernelGGL((merge_kernel<64, true>), grid, block, 0, stream, p, p.Lq);
+    else hipLaunchKernelGGL((merge_kernel<64, false>), grid, block, 0, stream, p, p.Lq);
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream) {

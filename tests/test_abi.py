@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8):
+    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9):
         assert F.status_str(s) and F.status_str(s) != "unknown status"
     assert F.status_str(12345) == "unknown status"
 
@@ -127,3 +127,19 @@ def test_global_check_validation():
     assert L.fabft_global_check(P, P, 0, 1, 8, 128, P, P) == F.E_SHAPE
     assert L.fabft_global_check(P, P, 1, 1, 0, 128, P, P) == F.E_SHAPE
     assert L.fabft_global_check(P + 2, P, 1, 1, 8, 128, P, P) == F.E_ALIGN
+
+
+def test_splitkv_workspace_size_and_validation():
+    L = F.lib()
+    assert L.fabft_splitkv_workspace_bytes(2, 3, 5, 128, 4) == 2 * 3 * 5 * 4 * (128 + 4) * 4
+    assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 64, 1) == (64 + 4) * 4
+    assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 96, 1) == F.E_HEADDIM
+    assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 128, 0) == F.E_SHAPE
+    assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 128, 65) == F.E_SHAPE
+    need = L.fabft_splitkv_workspace_bytes(1, 2, 8, 128, 4)
+    args = (P, P, P, P, P, P, 1, 2, 8, 8, 128, 1, 0.1)
+    assert L.fabft_attn_fwd_splitkv(*args, 4, None, need) == F.E_NULL
+    assert L.fabft_attn_fwd_splitkv(*args, 0, P, need) == F.E_SHAPE
+    assert L.fabft_attn_fwd_splitkv(*args, 65, P, need) == F.E_SHAPE
+    assert L.fabft_attn_fwd_splitkv(*args, 4, P + 8, need) == F.E_ALIGN
+    assert L.fabft_attn_fwd_splitkv(*args, 4, P, need - 1) == F.E_WORKSPACE
