@@ -60,7 +60,8 @@ enum {
 enum {
   FABFT_FLAG_RESID = 1,     /* |pred - actual| > tau_rel * M + tau_abs, where
                                M = sum_j |O_ij| + |pred| */
-  FABFT_FLAG_NONFINITE = 2, /* a residual is NaN or infinite */
+  FABFT_FLAG_NONFINITE = 2, /* a residual, or the row's sum_j |O_ij| (so the
+                               threshold), is NaN or infinite */
   FABFT_FLAG_WEIGHTED = 4   /* weighted check only (fabft_set_weighted_check):
                                |pred_w - actual_w| > tau_rel * M_w + tau_abs,
                                M_w = sum_j |O_ij| + |pred_w| */
@@ -124,6 +125,26 @@ void fabft_set_stream(void* hip_stream);
  */
 int fabft_set_threshold(float tau_rel, float tau_abs);
 void fabft_get_threshold(float* tau_rel, float* tau_abs);
+
+/*
+ * Recompute on flag (after detection): for every head (b, h) with a flagged
+ * row in `flags` (as written by any checked forward above on these q, k, v),
+ * run the checked forward again on that head alone, up to max_retries
+ * times, until none of its rows is flagged; O, resid and flags of the head
+ * are overwritten by the last run. A transient fault is then corrected; a
+ * head still flagged after max_retries is counted as persistent (its O is
+ * not trusted). Counts go to *n_recovered and *n_persistent.
+ * head_flags: device buffer of B*H bytes; head_flags_host: host buffer of
+ * B*H bytes (both caller-owned scratch; the library allocates nothing).
+ * Unlike the other entry points this one synchronises the library stream
+ * (it needs the flags on the host). max_retries >= 1.
+ */
+int fabft_recompute_flagged(const void* q, const void* k, const void* v,
+                            void* o, float* resid, uint8_t* flags,
+                            int B, int H, int Lq, int Lk, int d, int causal,
+                            float scale, uint8_t* head_flags,
+                            uint8_t* head_flags_host, int max_retries,
+                            int* n_recovered, int* n_persistent);
 
 /*
  * Global check per head (Algorithm 3, the check summed over all queries of

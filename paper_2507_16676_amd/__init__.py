@@ -75,6 +75,10 @@ def _load() -> ctypes.CDLL:
     L.fabft_attn_fwd_splitkv.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                          _f, _i, _vp, ctypes.c_longlong]
     L.fabft_attn_fwd_splitkv.restype = _i
+    L.fabft_recompute_flagged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                          _f, _vp, _vp, _i, ctypes.POINTER(_i),
+                                          ctypes.POINTER(_i)]
+    L.fabft_recompute_flagged.restype = _i
     L.fabft_global_check.argtypes = [_vp, _vp, _i, _i, _i, _i, _vp, _vp]
     L.fabft_global_check.restype = _i
     L.fabft_set_weighted_check.argtypes = [_i]
@@ -94,7 +98,8 @@ def _load() -> ctypes.CDLL:
 EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
            "fabft_attn_fwd_splitkv", "fabft_splitkv_workspace_bytes",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
-           "fabft_global_check", "fabft_set_weighted_check", "fabft_get_weighted_check",
+           "fabft_global_check", "fabft_recompute_flagged",
+           "fabft_set_weighted_check", "fabft_get_weighted_check",
            "fabft_key_tile", "fabft_query_tile", "fabft_status_str")
 
 
@@ -243,6 +248,28 @@ def attn_fwd_splitkv(q, k, v, causal: bool = False, scale: float | None = None,
     return o, resid, flags
 
 
+def recompute_flagged(q, k, v, o, resid, flags, causal: bool = False,
+                      scale: float | None = None, max_retries: int = 2):
+    """Re-run the checked forward on every head with a flagged row (in place,
+    up to max_retries times each). Returns (n_recovered, n_persistent)."""
+    import numpy as np
+    import torch
+    B, H, Lq, Lk, d = _shape(q, k, v)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    hf = torch.empty(B * H, dtype=torch.uint8, device=q.device)
+    hf_host = np.zeros(B * H, dtype=np.uint8)
+    nr, npers = ctypes.c_int(), ctypes.c_int()
+    _stream(q.device)
+    _check(_load().fabft_recompute_flagged(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                           resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
+                                           int(bool(causal)), scale, hf.data_ptr(),
+                                           hf_host.ctypes.data_as(ctypes.c_void_p),
+                                           int(max_retries), ctypes.byref(nr),
+                                           ctypes.byref(npers)),
+           "fabft_recompute_flagged")
+    return nr.value, npers.value
+
+
 def global_check(o, resid):
     """Per-head global check from attn_fwd's o and resid: returns (gsum [B, H]
     fp64 = sum of the row residuals, gflags [B, H] uint8)."""
@@ -313,7 +340,7 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
 
 __all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_splitkv", "splitkv_workspace_bytes",
            "splitkv_default_splits",
-           "global_check", "Fault", "FabftError", "set_threshold",
+           "global_check", "recompute_flagged", "Fault", "FabftError", "set_threshold",
            "get_threshold", "set_weighted_check", "get_weighted_check", "key_tile",
            "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "FLAG_RESID",
            "FLAG_NONFINITE", "FLAG_WEIGHTED"]

@@ -206,6 +206,55 @@ int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v, void* o,
   return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
 }
 
+int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o, float* resid,
+                            uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                            float scale, uint8_t* head_flags, uint8_t* head_flags_host,
+                            int max_retries, int* n_recovered, int* n_persistent) {
+  int n_qt = 0, grid = 0;
+  int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
+  if (rc != FABFT_OK) return rc;
+  if (!resid || !flags || !head_flags || !head_flags_host || !n_recovered || !n_persistent)
+    return FABFT_E_NULL;
+  if (max_retries < 1) return FABFT_E_SHAPE;
+  *n_recovered = 0;
+  *n_persistent = 0;
+  const int BH = B * H;
+  if (fabft::launch_head_flags(flags, BH, Lq, head_flags, g_stream) != 0) return FABFT_E_LAUNCH;
+  if (hipMemcpyAsync(head_flags_host, head_flags, (size_t)BH, hipMemcpyDeviceToHost, g_stream) !=
+          hipSuccess ||
+      hipStreamSynchronize(g_stream) != hipSuccess)
+    return FABFT_E_LAUNCH;
+  const size_t qstride = (size_t)Lq * d, kstride = (size_t)Lk * d;
+  for (int bh = 0; bh < BH; ++bh) {
+    if (!head_flags_host[bh]) continue;
+    // recompute this head alone (heads are independent) until its rows pass
+    const uint16_t* qh = static_cast<const uint16_t*>(q) + bh * qstride;
+    const uint16_t* kh = static_cast<const uint16_t*>(k) + bh * kstride;
+    const uint16_t* vh = static_cast<const uint16_t*>(v) + bh * kstride;
+    uint16_t* oh = static_cast<uint16_t*>(o) + bh * qstride;
+    float* rh = resid + (size_t)bh * Lq;
+    uint8_t* fh = flags + (size_t)bh * Lq;
+    bool clear = false;
+    for (int r = 0; r < max_retries && !clear; ++r) {
+      int n_qt1 = 0, grid1 = 0;
+      rc = validate(qh, kh, vh, oh, 1, 1, Lq, Lk, d, scale, &n_qt1, &grid1);
+      if (rc != FABFT_OK) return rc;
+      if (launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, scale, n_qt1, grid1), d, causal, 1) !=
+          FABFT_OK)
+        return FABFT_E_LAUNCH;
+      if (fabft::launch_head_flags(fh, 1, Lq, head_flags + bh, g_stream) != 0) return FABFT_E_LAUNCH;
+      if (hipMemcpyAsync(head_flags_host + bh, head_flags + bh, 1, hipMemcpyDeviceToHost,
+                         g_stream) != hipSuccess ||
+          hipStreamSynchronize(g_stream) != hipSuccess)
+        return FABFT_E_LAUNCH;
+      clear = head_flags_host[bh] == 0;
+    }
+    if (clear) ++*n_recovered;
+    else ++*n_persistent;
+  }
+  return FABFT_OK;
+}
+
 int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq, int d,
                        double* gsum, uint8_t* gflags) {
   if (!o || !resid || !gsum || !gflags) return FABFT_E_NULL;

@@ -45,6 +45,7 @@ inline int split_record_floats(int d) { return d + 4; }
 // Merge the partial states of every row (mode 3 writes them) into O, resid
 // and flags.
 int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream);
+int launch_head_flags(const uint8_t* flags, int BH, int Lq, uint8_t* hflags, hipStream_t stream);
 int launch_global(const uint16_t* o, const float* resid, int BH, int Lq, int d, float tau_rel,
                   float tau_abs, double* gsum, uint8_t* gflag, hipStream_t stream);
 

@@ -650,8 +650,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     const float r = pred - act;
     const float M = absum + __builtin_fabsf(pred);
     // non-finite test on the bits (this file is built with relaxed NaN rules);
-    // a non-finite residual also fails the threshold comparison
-    bool nonfinite = nonfinite_bits(r);
+    // a non-finite residual also fails the threshold comparison. An overflow
+    // of sum_j |O_ij| (a huge but finite row) would make the threshold
+    // infinite and pass any residual, so it counts as non-finite as well.
+    bool nonfinite = nonfinite_bits(r) || nonfinite_bits(absum);
     uint8_t f = (__builtin_fabsf(r) <= p.tau_rel * M + p.tau_abs) ? 0 : 1;
     // weighted check: pred_w = c_w / l against sum_j (-1)^j O_ij (the same
     // threshold rule; |w_j| = 1 keeps M)
@@ -769,7 +771,8 @@ __global__ __launch_bounds__(64 * kMergeWaves) void merge_kernel(FwdParams p, in
   absum = wave_sum(absum);
   const float pred = c * inv;
   const float r = pred - act;
-  bool nonfinite = nonfinite_bits(r);
+  // as in the forward epilogue: an overflowed sum_j |O_ij| counts as non-finite
+  bool nonfinite = nonfinite_bits(r) || nonfinite_bits(absum);
   uint8_t f = (__builtin_fabsf(r) <= p.tau_rel * (absum + __builtin_fabsf(pred)) + p.tau_abs) ? 0 : 1;
   if constexpr (WCHK) {
     act_w = wave_sum(act_w);
@@ -855,6 +858,29 @@ __global__ __launch_bounds__(kGThreads) void global_check_kernel(
     gsum[bh] = R;
     gflag[bh] = f;
   }
+}
+
+// ---- per-head OR of the row flags (one workgroup per head)
+__global__ __launch_bounds__(kGThreads) void head_flags_kernel(const uint8_t* __restrict__ flags,
+                                                             int Lq, uint8_t* __restrict__ hflags) {
+  __shared__ uint32_t red[kGThreads];
+  const int bh = blockIdx.x;
+  const uint8_t* f = flags + (size_t)bh * Lq;
+  uint32_t acc = 0;
+  for (int i = threadIdx.x; i < Lq; i += kGThreads) acc |= f[i];
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  for (int s = kGThreads / 2; s > 0; s >>= 1) {
+    if ((int)threadIdx.x < s) red[threadIdx.x] |= red[threadIdx.x + s];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) hflags[bh] = (uint8_t)red[0];
+}
+
+int launch_head_flags(const uint8_t* flags, int BH, int Lq, uint8_t* hflags, hipStream_t stream) {
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(head_flags_kernel, dim3(BH), dim3(kGThreads), 0, stream, flags, Lq, hflags);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 int launch_global(const uint16_t* o, const float* resid, int BH, int Lq, int d, float tau_rel,

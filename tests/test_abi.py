@@ -143,3 +143,18 @@ def test_splitkv_workspace_size_and_validation():
     assert L.fabft_attn_fwd_splitkv(*args, 65, P, need) == F.E_SHAPE
     assert L.fabft_attn_fwd_splitkv(*args, 4, P + 8, need) == F.E_ALIGN
     assert L.fabft_attn_fwd_splitkv(*args, 4, P, need - 1) == F.E_WORKSPACE
+
+
+def test_recompute_flagged_validation():
+    L = F.lib()
+    n1, n2 = ctypes.c_int(7), ctypes.c_int(7)
+    base = (P, P, P, P, P, P, 1, 2, 8, 8, 128, 0, 0.1)
+    ok = (P, P, 2, ctypes.byref(n1), ctypes.byref(n2))
+    assert L.fabft_recompute_flagged(*base, *ok[:2], 0, *ok[3:]) == F.E_SHAPE
+    assert L.fabft_recompute_flagged(*base, None, P, 2, *ok[3:]) == F.E_NULL
+    assert L.fabft_recompute_flagged(*base, P, None, 2, *ok[3:]) == F.E_NULL
+    assert L.fabft_recompute_flagged(*base, P, P, 2, None, ctypes.byref(n2)) == F.E_NULL
+    bad_d = base[:10] + (96,) + base[11:]
+    assert L.fabft_recompute_flagged(*bad_d, *ok) == F.E_HEADDIM
+    no_flags = base[:5] + (None,) + base[6:]
+    assert L.fabft_recompute_flagged(*no_flags, *ok) == F.E_NULL

@@ -77,6 +77,20 @@ def test_p_site_flip(golden):
     assert int(flags.sum()) == int(flags[0, 0, 250])
 
 
+def test_p_exponent_msb_flips_on_short_rows_are_flagged(golden):
+    """Flipping the top exponent bit of p~ in the first key tile of a short
+    row scales it by 2^128: O stays finite in bf16 but sum_j |O_ij| overflows
+    fp32, which would make the threshold infinite. Every such row must still
+    be flagged."""
+    (_, (o0, r0, f0, p0, a0)) = golden
+    row = 20
+    for key in range(0, row + 1, 3):
+        f = F.Fault("P", b=0, h=1, row=row, col=key, bit=14)
+        o, resid, flags, pred, actual = _inject(golden, f)
+        assert _changed_rows(o, o0) == {(0, 1, row)}, key
+        assert int(flags[0, 1, row]) & F.FLAG_RESID, (key, float(resid[0, 1, row]))
+
+
 def test_v_site_flip(golden):
     # key 100, column 5, in the workgroup holding the second query tile
     qt = F.query_tile()
