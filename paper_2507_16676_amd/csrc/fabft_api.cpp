@@ -35,6 +35,9 @@ int validate(const void* q, const void* k, const void* v, void* o, int B, int H,
   if (!q || !k || !v || !o) return FABFT_E_NULL;
   if (d != 64 && d != 128) return FABFT_E_HEADDIM;
   if (B < 1 || H < 1 || Lq < 1 || Lk < 1) return FABFT_E_SHAPE;
+  // K and V of one head are addressed with 32-bit byte offsets (one key tile
+  // of slack for the last tile's reads)
+  if ((static_cast<long long>(Lk) + 64) * d * 2 > 0xffffffffLL) return FABFT_E_SHAPE;
   if (!std::isfinite(scale) || scale < 0.f) return FABFT_E_SCALE;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return FABFT_E_ALIGN;
   const long long nqt = (static_cast<long long>(Lq) + fabft::kQueryTile - 1) / fabft::kQueryTile;

@@ -17,7 +17,7 @@
 //    work plus one exchange between lane i and lane i+32 (permlane32 swap).
 //  * Q stays in VGPRs as MFMA B operands for the whole pass.
 //  * K and V tiles go from global memory straight into a 4-stage LDS ring
-//    (global_load_lds_dwordx4: lane l of a load lands at base + 16 l), three
+//    (buffer_load_dwordx4 ... lds: lane l of a load lands at base + 16 l), three
 //    tiles ahead of use, with no register staging. Both tiles are stored
 //    row-major with their 16-byte chunks XOR-swizzled by row: the K
 //    swizzle makes the MFMA operand reads conflict-free, the V swizzle makes
@@ -144,15 +144,37 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt(N | (0x7 << 4) | (0xF << 8));
 }
 
-// global_load_lds_dwordx4 as inline asm: the 16 bytes at gptr of lane l land
-// at LDS address lds + 16 l (lds is wave-uniform and goes through m0). The
-// compiler does not see this load, so it adds no wait of its own before LDS
-// reads: its tracking of the builtin form makes every transposed V read wait
-// for all outstanding loads, the prefetched tiles included. wait_vmcnt and
-// the workgroup barrier are what order these loads before their readers.
-__device__ __forceinline__ void load_lds16(const void* gptr, lds_void* lds) {
+// buffer_load_dwordx4 ... lds through a buffer resource (base, size in
+// bytes): the 16 bytes at byte offset voff + soff of lane l land at LDS
+// address lds + 16 l (lds is wave-uniform and goes through m0), and a load at
+// or past the size reads zeros. The per-lane offsets stay fixed while the
+// tile moves in the scalar soff, so issuing a tile costs no vector
+// instruction, and rows past the end of K and V need no clamping.
+// Inline asm: the compiler does not see this load, so it adds no wait of its
+// own before LDS reads (its tracking of the builtin form makes every
+// transposed V read wait for all outstanding loads, the prefetched tiles
+// included); wait_vmcnt and the workgroup barrier order these loads before
+// their readers. For the same reason it inserts no hazard wait states before
+// the asm: a vector instruction that writes an SGPR (v_readfirstlane, or
+// v_readlane restoring a spilled descriptor) needs 5 wait states before a
+// memory instruction reads that SGPR, so the asm starts with s_nop 4 (which
+// also covers the write of m0 before an LDS transfer).
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)(uintptr_t)base;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((a >> 32) & 0xffffu));   // stride 0
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;   // 32-bit data format, raw (offset) addressing
+  return r;
+}
+__device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, uint32_t soff,
+                                                  lds_void* lds) {
   const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" : : "v"(gptr), "{m0}"(base) : "memory");
+  const uint32_t so = __builtin_amdgcn_readfirstlane(soff);
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+               : : "v"(voff), "s"(rsrc), "s"(so), "{m0}"(base) : "memory");
 }
 
 // Tile layouts in LDS. A tile row (one key) holds D bf16 = CPR 16-byte
@@ -176,11 +198,20 @@ struct Tile {
 enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRowWLo = 5,
        kVsmRows = 6 };
 
+// The ring's K tiles, then its V tiles, then the small operands: with the
+// stage a compile-time constant, every operand read of a tile is a per-lane
+// base register plus an immediate offset (K and V stages each span 64 KiB at
+// d = 128, the reach of the LDS offset field).
 template <int D>
-struct Stage {
-  uint16_t k[kBc * D];
-  uint16_t v[kBc * D];
-  uint16_t vsm[kVsmRows][kBc];
+struct Ring {
+  uint16_t k[kStages][kBc * D];
+  uint16_t v[kStages][kBc * D];
+  uint16_t vsm[kStages][kVsmRows][kBc];
+};
+
+template <int S>
+struct StageId {
+  static constexpr int value = S;
 };
 
 // WCHK: the weighted second checksum is compiled in (only with CHECK).
@@ -196,7 +227,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   static_assert(NLD >= 1 && BC * CPR == NLD * kThreads, "loads cover the tile");
   static_assert(kThreads == BC * 8 && CPR % 8 == 0, "sumrow: 8 threads per key");
 
-  __shared__ __attribute__((aligned(16))) Stage<D> stage[kStages];
+  __shared__ __attribute__((aligned(16))) Ring<D> ring;
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -274,7 +305,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   // prologue barrier)
   {
     const int st_i = tid >> 7, row = kRowOnes + ((tid >> 6) & 1), key = tid & 63;
-    stage[st_i].vsm[row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
+    ring.vsm[st_i][row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
   }
   // row of the c / l operand that MFMA row mrow reads (rows 0, 1 only with
   // the checksum, rows 8, 9 only with the weighted one)
@@ -285,38 +316,43 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
                                                : (int)kRowZero;
 
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
-  // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk repeat
-  // row Lk-1 (finite values that the mask gives weight 0)
-  const uint16_t* kg = p.k + kbase;
-  const uint16_t* vg = p.v + kbase;
-  auto issue = [&](int t) {
+  // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk read as
+  // zeros (the mask gives them weight 0)
+  const i32x4 krs = buffer_rsrc(p.k + kbase, (uint32_t)Lk * D * 2);
+  const i32x4 vrs = buffer_rsrc(p.v + kbase, (uint32_t)Lk * D * 2);
+  uint32_t kvo[NLD], vvo[NLD];
+#pragma unroll
+  for (int j = 0; j < NLD; ++j) {
+    const int slot = j * kThreads + tid;
+    const int row = slot / CPR, sc = slot % CPR;
+    kvo[j] = (uint32_t)(row * D + 8 * (sc ^ Tile<D>::kswz(row))) * 2;
+    vvo[j] = (uint32_t)(row * D + 8 * (sc ^ Tile<D>::vswz(row))) * 2;
+  }
+  auto issue = [&](auto S_, int t) {
+    constexpr int S = decltype(S_)::value;
     if (t >= t_end) return;
-    Stage<D>& st = stage[t % kStages];
-    const int kv0 = t * BC;
+    const uint32_t soff = (uint32_t)t * BC * D * 2;
 #pragma unroll
     for (int j = 0; j < NLD; ++j) {
-      const int slot = j * kThreads + tid;
-      const int row = slot / CPR, sc = slot % CPR;
-      const int grow = min(kv0 + row, Lk - 1);
-      const uint16_t* ks = kg + (size_t)grow * D + 8 * (sc ^ Tile<D>::kswz(row));
-      const uint16_t* vsrc = vg + (size_t)grow * D + 8 * (sc ^ Tile<D>::vswz(row));
       // each wave writes its own contiguous 1 KiB of the stage
       const int wbase = (j * kThreads + 64 * wave) * 8;
-      load_lds16(ks, (lds_void*)(st.k + wbase));
-      load_lds16(vsrc, (lds_void*)(st.v + wbase));
+      buffer_load_lds16(krs, kvo[j], soff, (lds_void*)(ring.k[S] + wbase));
+      buffer_load_lds16(vrs, vvo[j], soff, (lds_void*)(ring.v[S] + wbase));
     }
   };
 
   // ---- sumrow(V) of the tile in stage `buf` (Eq. 4): 8 threads per key
-  auto sumrow = [&](int buf, int t) {
-    Stage<D>& st = stage[buf];
+  auto sumrow = [&](auto S_, int t) {
+    constexpr int S = decltype(S_)::value;
+    uint16_t* const sv = ring.v[S];
+    uint16_t(*const svsm)[kBc] = ring.vsm[S];
     const int key = tid >> 3, part = tid & 7;
     constexpr int CPT = CPR / 8;   // chunks per thread
     float a = 0.f, aw = 0.f;
     u32x4 ch[CPT];
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      ch[i] = *reinterpret_cast<const u32x4*>(&st.v[Tile<D>::vidx(key, CPT * part + i)]);
+      ch[i] = *reinterpret_cast<const u32x4*>(&sv[Tile<D>::vidx(key, CPT * part + i)]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) a = dot2(ch[i][e], kOnes, a);
     }
@@ -334,14 +370,14 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
       const float hif = __uint_as_float(hi << 16);
       const uint32_t lo = pack_bf16x2(vs - hif, 0.f) & 0xffffu;
-      st.vsm[kRowVsHi][key] = (uint16_t)hi;
-      st.vsm[kRowVsLo][key] = (uint16_t)lo;
+      svsm[kRowVsHi][key] = (uint16_t)hi;
+      svsm[kRowVsLo][key] = (uint16_t)lo;
       if constexpr (WCHK) {
         const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
         const float whif = __uint_as_float(whi << 16);
         const uint32_t wlo = pack_bf16x2(vw - whif, 0.f) & 0xffffu;
-        st.vsm[kRowWHi][key] = (uint16_t)whi;
-        st.vsm[kRowWLo][key] = (uint16_t)wlo;
+        svsm[kRowWHi][key] = (uint16_t)whi;
+        svsm[kRowWLo][key] = (uint16_t)wlo;
       }
     }
     if constexpr (INJECT) {
@@ -359,7 +395,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
               for (int ee = 0; ee < 4; ++ee)
                 if (ee == e) w[ee] ^= mask;
-              *reinterpret_cast<u32x4*>(&st.v[Tile<D>::vidx(key, c)]) = w;
+              *reinterpret_cast<u32x4*>(&sv[Tile<D>::vidx(key, c)]) = w;
             }
         }
       }
@@ -367,8 +403,11 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   };
 
   // ---- one key tile for this wave (steps A1-A5)
-  auto compute = [&](int t) {
-    const Stage<D>& st = stage[t % kStages];
+  auto compute = [&](auto S_, int t) {
+    constexpr int S = decltype(S_)::value;
+    const uint16_t* const sk = ring.k[S];
+    const uint16_t* const sv = ring.v[S];
+    const uint16_t(*const svsm)[kBc] = ring.vsm[S];
     const int kv0 = t * BC;
     const bool need_mask = (kv0 + BC > Lk) || (CAUSAL && kv0 + BC - 1 > wq_lo + off);
 
@@ -382,7 +421,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     constexpr int NQK = NDS * NKB, KAHEAD = 6;
     auto kread = [&](int i) {
       return *reinterpret_cast<const u32x4*>(
-          &st.k[Tile<D>::kidx((i % NKB) * 32 + krow, 2 * (i / NKB) + grp)]);
+          &sk[Tile<D>::kidx((i % NKB) * 32 + krow, 2 * (i / NKB) + grp)]);
     };
     u32x4 kop[NQK];
 #pragma unroll
@@ -421,12 +460,13 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
           if (!ok) sacc[kb][i] = -__builtin_inff();
         }
     }
-    float mx = -__builtin_inff();
+    // one chain of three-input maxima (v_max3): one instruction per two scores
+    float mx = __builtin_fmaxf(sacc[0][0], sacc[0][1]);
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-      for (int i = 0; i < 16; i += 2)
-        mx = __builtin_fmaxf(mx, __builtin_fmaxf(sacc[kb][i], sacc[kb][i + 1]));
+      for (int i = (kb == 0 ? 2 : 0); i < 16; i += 2)
+        mx = __builtin_fmaxf(__builtin_fmaxf(mx, sacc[kb][i]), sacc[kb][i + 1]);
     mx = max_xor32(mx);
     // lazy running max in the exp2 domain
     const float mt2 = (mx == -__builtin_inff()) ? -__builtin_inff() : mx * sl2;
@@ -480,7 +520,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(&st.vsm[vsm_row][32 * kb + 16 * h + 8 * grp]);
+        const u32x4 a = *reinterpret_cast<const u32x4*>(&svsm[vsm_row][32 * kb + 16 * h + 8 * grp]);
         aux = mfma32(a, pb[kb][h], aux);
       }
     if constexpr (INJECT) {
@@ -528,7 +568,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
         const int key = 32 * kb + 16 * h + 4 * t2 + tr_key;
         const int col = 32 * db + tr_col;
         const int idx = Tile<D>::vidx(key, col >> 3) + (col & 7);
-        const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(st.v + idx));
+        const s16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(sv + idx));
         part[t2] = __builtin_bit_cast(u32x2, r);
       }
       return u32x4{part[0][0], part[0][1], part[1][0], part[1][1]};
@@ -564,23 +604,27 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 
   // ---- pipeline: tiles t+1 and t+2 in flight while tile t is processed
   constexpr int LPT = 2 * NLD;   // loads per thread per tile (K and V)
+  // tile t sits in stage (t - t_lo) % kStages; the loop below is unrolled
+  // kStages times so that each copy knows its stages at compile time
   if (t_end > t_lo) {
-    issue(t_lo);
-    issue(t_lo + 1);
-    issue(t_lo + 2);
+    issue(StageId<0>(), t_lo);
+    issue(StageId<1>(), t_lo + 1);
+    issue(StageId<2>(), t_lo + 2);
     // first tile complete; the next two may be outstanding
     if (t_end - t_lo >= 3) wait_vmcnt<2 * LPT>();
     else if (t_end - t_lo == 2) wait_vmcnt<LPT>();
     else wait_vmcnt<0>();
     __syncthreads();
-    if constexpr (CHECK) sumrow(t_lo % kStages, t_lo);
+    if constexpr (CHECK) sumrow(StageId<0>(), t_lo);
   }
   // A use of Q here, on every path into the loop, puts the compiler's own
   // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
   // also waits for tiles 1 and 2) before the loop rather than inside it.
 #pragma unroll
   for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
-  for (int t = t_lo; t < t_end; ++t) {
+  static_assert(kStages == 4, "the loop below is unrolled over four stages");
+  auto step = [&](auto S_, int t) {
+    constexpr int S = decltype(S_)::value;
     // tile t+1 complete (tile t+2 may still be in flight); after the barrier
     // every wave is done with tile t-1, whose stage takes tile t+3
     if (t + 2 < t_end) wait_vmcnt<LPT>();
@@ -588,12 +632,20 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     __syncthreads();
     // waves whose rows see none of this tile's keys, or that hold no row
     // below Lq, skip it (they still load and take sumrow for the others)
-    if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(t);
-    issue(t + 3);
+    if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(S_, t);
+    issue(StageId<(S + 3) % kStages>(), t + 3);
     if constexpr (CHECK) {
-      if (t + 1 < t_end) sumrow((t + 1) % kStages, t + 1);
+      if (t + 1 < t_end) sumrow(StageId<(S + 1) % kStages>(), t + 1);
     }
-
+  };
+  for (int t = t_lo; t < t_end; t += kStages) {
+    step(StageId<0>(), t);
+    if (t + 1 >= t_end) break;
+    step(StageId<1>(), t + 1);
+    if (t + 2 >= t_end) break;
+    step(StageId<2>(), t + 2);
+    if (t + 3 >= t_end) break;
+    step(StageId<3>(), t + 3);
   }
 
   if constexpr (SPLIT) {
