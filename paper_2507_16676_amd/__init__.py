@@ -26,8 +26,8 @@ _vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
 _fp = ctypes.POINTER(ctypes.c_float)
 
 FABFT_OK = 0
-E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE = \
-    -1, -2, -3, -4, -5, -6, -7, -8, -9
+E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE, \
+    E_ALLOC = -1, -2, -3, -4, -5, -6, -7, -8, -9, -10
 FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED = 1, 2, 4
 SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M = 0, 1, 2, 3, 4, 5, 6, 7
 SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V,

@@ -38,6 +38,8 @@ int validate(const void* q, const void* k, const void* v, void* o, int B, int H,
   // K and V of one head are addressed with 32-bit byte offsets (one key tile
   // of slack for the last tile's reads)
   if ((static_cast<long long>(Lk) + 64) * d * 2 > 0xffffffffLL) return FABFT_E_SHAPE;
+  // one operand record per (head, key tile), indexed in 32 bits
+  if (static_cast<long long>(B) * H * fabft::vrec_tiles(Lk) > INT_MAX) return FABFT_E_SHAPE;
   if (!std::isfinite(scale) || scale < 0.f) return FABFT_E_SCALE;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return FABFT_E_ALIGN;
   const long long nqt = (static_cast<long long>(Lq) + fabft::kQueryTile - 1) / fabft::kQueryTile;
@@ -67,6 +69,8 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.nsplit = 1;
   p.split_tiles = 0;
   p.ws = nullptr;
+  p.vrec = nullptr;
+  p.ntk = 0;
   p.Lq = Lq;
   p.Lk = Lk;
   p.n_qt = n_qt;
@@ -79,7 +83,48 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   return p;
 }
 
-int launch(const fabft::FwdParams& p, int d, int causal, int mode) {
+// Operand records of the checked forward (sumrow(V) of every key, written by
+// a pre-pass): one buffer per device, allocated on first use, replaced by a
+// larger one when a call needs more, kept until the process ends.
+constexpr int kMaxDevices = 64;
+void* g_rec[kMaxDevices] = {};
+size_t g_rec_bytes[kMaxDevices] = {};
+
+uint16_t* rec_buffer(size_t bytes) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+  if (g_rec_bytes[dev] < bytes) {
+    if (g_rec[dev]) {
+      // launches on any stream may still read the old buffer
+      if (hipDeviceSynchronize() != hipSuccess) return nullptr;
+      (void)hipFree(g_rec[dev]);
+      g_rec[dev] = nullptr;
+      g_rec_bytes[dev] = 0;
+    }
+    void* ptr = nullptr;
+    if (hipMalloc(&ptr, bytes) != hipSuccess) return nullptr;
+    g_rec[dev] = ptr;
+    g_rec_bytes[dev] = bytes;
+  }
+  return static_cast<uint16_t*>(g_rec[dev]);
+}
+
+// sumrow(V) records of the BH heads of p, on the library stream
+int prepare_records(fabft::FwdParams& p, int BH, int d) {
+  uint16_t* rec = rec_buffer(static_cast<size_t>(fabft::vrec_bytes(BH, p.Lk)));
+  if (!rec) return FABFT_E_ALLOC;
+  if (fabft::launch_vrec(p.v, BH, p.Lk, d, rec, g_stream) != 0) return FABFT_E_LAUNCH;
+  p.vrec = rec;
+  p.ntk = static_cast<int>(fabft::vrec_tiles(p.Lk));
+  return FABFT_OK;
+}
+
+// mode 0: no checksum; 1: checksum; 2: checksum + injection/debug
+int launch(fabft::FwdParams p, int d, int causal, int mode, int BH) {
+  if (mode != 0) {
+    const int rc = prepare_records(p, BH, d);
+    if (rc != FABFT_OK) return rc;
+  }
   const int rc = fabft::launch_fwd(p, d, causal != 0, mode, g_stream);
   return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
 }
@@ -95,7 +140,8 @@ int fabft_attn_fwd(const void* q, const void* k, const void* v, void* o, float* 
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   if (!resid || !flags) return FABFT_E_NULL;
-  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid), d, causal, 1);
+  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid), d, causal, 1,
+                B * H);
 }
 
 int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o, int B, int H,
@@ -104,7 +150,7 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   return launch(make_params(q, k, v, o, nullptr, nullptr, Lq, Lk, scale, n_qt, grid), d,
-                causal, 0);
+                causal, 0, B * H);
 }
 
 int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,
@@ -158,7 +204,7 @@ int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, 
     p.f_tile = f->tile;
     p.f_bit = f->bit;
   }
-  return launch(p, d, causal, 2);
+  return launch(p, d, causal, 2, B * H);
 }
 
 void fabft_set_stream(void* hip_stream) { g_stream = static_cast<hipStream_t>(hip_stream); }
@@ -203,6 +249,8 @@ int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v, void* o,
   p.split_tiles = (tiles + nsplit - 1) / nsplit;
   p.ws = static_cast<float*>(workspace);
   p.grid = static_cast<int>(g);
+  rc = prepare_records(p, B * H, d);
+  if (rc != FABFT_OK) return rc;
   rc = fabft::launch_fwd(p, d, causal != 0, 3, g_stream);
   if (rc != 0) return FABFT_E_LAUNCH;
   rc = fabft::launch_merge(p, d, B * H, g_stream);
@@ -242,9 +290,8 @@ int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o
       int n_qt1 = 0, grid1 = 0;
       rc = validate(qh, kh, vh, oh, 1, 1, Lq, Lk, d, scale, &n_qt1, &grid1);
       if (rc != FABFT_OK) return rc;
-      if (launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, scale, n_qt1, grid1), d, causal, 1) !=
-          FABFT_OK)
-        return FABFT_E_LAUNCH;
+      rc = launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, scale, n_qt1, grid1), d, causal, 1, 1);
+      if (rc != FABFT_OK) return rc;
       if (fabft::launch_head_flags(fh, 1, Lq, head_flags + bh, g_stream) != 0) return FABFT_E_LAUNCH;
       if (hipMemcpyAsync(head_flags_host + bh, head_flags + bh, 1, hipMemcpyDeviceToHost,
                          g_stream) != hipSuccess ||
@@ -293,6 +340,7 @@ const char* fabft_status_str(int status) {
     case FABFT_E_FAULT: return "fault descriptor out of range";
     case FABFT_E_THRESHOLD: return "threshold must be >= 0";
     case FABFT_E_WORKSPACE: return "workspace too small (see fabft_splitkv_workspace_bytes)";
+    case FABFT_E_ALLOC: return "device memory allocation failed (sumrow buffer)";
     default: return "unknown status";
   }
 }

@@ -8,6 +8,15 @@
 namespace fabft {
 
 constexpr int kQueryTile = 256;  // query rows per workgroup
+constexpr int kKeyTile = 64;     // keys per tile
+// Per key tile of a head: the small A operand of the c / l product, 8 rows
+// of kKeyTile bf16 (sumrow(V) hi, lo, ones, zeros, weighted sum hi, lo,
+// zeros, zeros), written by launch_vrec before a checked forward.
+constexpr int kRecElems = 8 * kKeyTile;
+inline long long vrec_tiles(int Lk) { return (Lk + kKeyTile - 1) / kKeyTile; }
+inline long long vrec_bytes(long long BH, int Lk) {
+  return BH * vrec_tiles(Lk) * kRecElems * 2;
+}
 
 struct FwdParams {
   const uint16_t* q;
@@ -27,6 +36,8 @@ struct FwdParams {
   int nsplit;
   int split_tiles;
   float* ws;
+  const uint16_t* vrec;  // operand records of every head (checked modes)
+  int ntk;               // key tiles per head in vrec
   int Lq, Lk;
   int n_qt;       // query tiles per head
   int grid;       // workgroups = B * H * n_qt
@@ -39,6 +50,8 @@ struct FwdParams {
 // 3: checksum on, one key split per workgroup (partial states to p.ws)
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream);
 int key_tile(int d);
+// sumrow(V) records of BH heads (Eq. 4) into rec (vrec_bytes(BH, Lk) bytes).
+int launch_vrec(const uint16_t* v, int BH, int Lk, int d, uint16_t* rec, hipStream_t stream);
 // Partial-state record of (head, row, split) in the split workspace, in
 // floats: m (exp2 domain), l, c, c_w, then the d unnormalised outputs o.
 inline int split_record_floats(int d) { return d + 4; }

@@ -30,17 +30,19 @@
 //  * The K rows feeding MFMA row r are permuted (bits 2 and 3 of r swapped)
 //    so that the S^T accumulator of a lane already holds, for each 16-key
 //    step of P V, the 8 consecutive keys its B operand needs.
-//  * sumrow(V) of tile t+1 is computed from LDS by the whole workgroup while
-//    tile t is processed (8 threads per key, fp32 via v_dot2 and a DPP
-//    reduction) and stored as a bf16 pair hi + lo (hi = bf16(vs),
-//    lo = bf16(vs - hi); |vs - hi - lo| <= 2^-17|vs|): one sum per key and
-//    tile shared by the 256 rows, the paper's shared adder.
+//  * sumrow(V) of every key is computed once per head by vrec_kernel (8
+//    threads per key, fp32 via v_dot2 and a DPP reduction) and stored as a
+//    bf16 pair hi + lo (hi = bf16(vs), lo = bf16(vs - hi);
+//    |vs - hi - lo| <= 2^-17|vs|): one sum per key shared by all query rows,
+//    the paper's shared adder. It reaches the forward kernel as an 8-row
+//    operand record per key tile [sumrow hi; sumrow lo; ones; 0; weighted
+//    hi; weighted lo; 0; 0], loaded into LDS with the K and V tiles.
 //  * The weights p~ = bf16(p) feed the P V MFMA; l and the checksum c use
 //    exactly those p~, so that the rounding of P cancels between pred and
 //    actual. They come from one more 32x32x16 MFMA per 16-key step with the
-//    same P^T operand and a 4-row A operand [sumrow hi; sumrow lo; ones; 0]
-//    held in LDS: rows 0-2 of that accumulator are c_hi, c_lo and l of each
-//    query, rescaled like o (Eq. 10 carries c as an extra row of V^T).
+//    same P^T operand and that record as A operand: rows 0-2 of the
+//    accumulator are c_hi, c_lo and l of each query, rescaled like o (Eq. 10
+//    carries c as an extra row of V^T).
 //  * Lazy rescaling: the running max used for the exponentials is moved only
 //    when a tile's max exceeds it by more than 8 in the exp2 domain, so
 //    p <= 256 and o, l, c are rescaled (alpha != 1) rarely; o*alpha is
@@ -170,8 +172,8 @@ __device__ __forceinline__ i32x4 buffer_rsrc(const void* base, uint32_t bytes) {
   return r;
 }
 __device__ __forceinline__ void buffer_load_lds16(i32x4 rsrc, uint32_t voff, uint32_t soff,
-                                                  lds_void* lds) {
-  const uint32_t base = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)lds);
+                                                  uint32_t lds) {
+  const uint32_t base = __builtin_amdgcn_readfirstlane(lds);
   const uint32_t so = __builtin_amdgcn_readfirstlane(soff);
   asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
                : : "v"(voff), "s"(rsrc), "s"(so), "{m0}"(base) : "memory");
@@ -192,11 +194,13 @@ struct Tile {
 
 // Rows of the small A operand that yields c and l: sumrow(V) as bf16 hi and
 // lo parts, ones, zeros, and the weighted row sums sum_j (-1)^j V_kj as hi
-// and lo parts. MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9
-// read WHi, WLo (accumulator elements 4, 5 of lanes 0-31); the others read
-// the zero row.
+// and lo parts, padded to 8 rows (1 KiB per key tile: one wave-wide 16-byte
+// load). MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9 read
+// WHi, WLo (accumulator elements 4, 5 of lanes 0-31); the others read the
+// zero row. vrec_kernel writes this operand for every key tile of a head.
 enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRowWLo = 5,
-       kVsmRows = 6 };
+       kVsmRows = 8 };
+static_assert(kVsmRows * kBc == kRecElems && kBc == kKeyTile, "operand record layout");
 
 // The ring's K tiles, then its V tiles, then the small operands: with the
 // stage a compile-time constant, every operand read of a tile is a per-lane
@@ -225,7 +229,6 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   constexpr int NDS = D / 16;     // 16-wide steps over d in Q K^T
   constexpr int NLD = BC * CPR / kThreads;   // 16-byte loads per thread per tensor and tile
   static_assert(NLD >= 1 && BC * CPR == NLD * kThreads, "loads cover the tile");
-  static_assert(kThreads == BC * 8 && CPR % 8 == 0, "sumrow: 8 threads per key");
 
   __shared__ __attribute__((aligned(16))) Ring<D> ring;
 
@@ -301,9 +304,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   float m2_run = -__builtin_inff();   // running max, exp2 domain (s * scale * log2 e)
   const float sl2 = p.sl2;
 
-  // constant rows of the c / l operand in every stage (visible after the
+  // without the checksum no record is loaded: the ones and zero rows of the
+  // c / l operand (l only) are set once in every stage (visible after the
   // prologue barrier)
-  {
+  if constexpr (!CHECK) {
     const int st_i = tid >> 7, row = kRowOnes + ((tid >> 6) & 1), key = tid & 63;
     ring.vsm[st_i][row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
   }
@@ -320,6 +324,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   // zeros (the mask gives them weight 0)
   const i32x4 krs = buffer_rsrc(p.k + kbase, (uint32_t)Lk * D * 2);
   const i32x4 vrs = buffer_rsrc(p.v + kbase, (uint32_t)Lk * D * 2);
+  // the operand record of each key tile (1 KiB) is loaded by one wave
+  constexpr int kRecWave = kWaves - 1;
+  const i32x4 rrs = buffer_rsrc(CHECK ? p.vrec + (size_t)bh * p.ntk * kRecElems : p.v,
+                                CHECK ? (uint32_t)p.ntk * kRecElems * 2 : 0u);
   uint32_t kvo[NLD], vvo[NLD];
 #pragma unroll
   for (int j = 0; j < NLD; ++j) {
@@ -328,77 +336,30 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     kvo[j] = (uint32_t)(row * D + 8 * (sc ^ Tile<D>::kswz(row))) * 2;
     vvo[j] = (uint32_t)(row * D + 8 * (sc ^ Tile<D>::vswz(row))) * 2;
   }
+  // LDS byte address of the ring and of this wave's 1 KiB slot in a tile
+  const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void*)&ring;
+  const uint32_t wave_lds = __builtin_amdgcn_readfirstlane(ring_lds + 1024u * wave);
   auto issue = [&](auto S_, int t) {
     constexpr int S = decltype(S_)::value;
     if (t >= t_end) return;
     const uint32_t soff = (uint32_t)t * BC * D * 2;
+    // opaque copy: the destination addresses are formed here from one SGPR
+    // (scalar adds) rather than hoisted as one live SGPR per stage and load
+    uint32_t wl = wave_lds;
+    asm volatile("" : "+s"(wl));
 #pragma unroll
     for (int j = 0; j < NLD; ++j) {
       // each wave writes its own contiguous 1 KiB of the stage
-      const int wbase = (j * kThreads + 64 * wave) * 8;
-      buffer_load_lds16(krs, kvo[j], soff, (lds_void*)(ring.k[S] + wbase));
-      buffer_load_lds16(vrs, vvo[j], soff, (lds_void*)(ring.v[S] + wbase));
+      constexpr uint32_t kOff = offsetof(Ring<D>, k) + S * sizeof(Ring<D>::k[0]);
+      constexpr uint32_t vOff = offsetof(Ring<D>, v) + S * sizeof(Ring<D>::v[0]);
+      buffer_load_lds16(krs, kvo[j], soff, wl + kOff + j * kThreads * 16);
+      buffer_load_lds16(vrs, vvo[j], soff, wl + vOff + j * kThreads * 16);
     }
-  };
-
-  // ---- sumrow(V) of the tile in stage `buf` (Eq. 4): 8 threads per key
-  auto sumrow = [&](auto S_, int t) {
-    constexpr int S = decltype(S_)::value;
-    uint16_t* const sv = ring.v[S];
-    uint16_t(*const svsm)[kBc] = ring.vsm[S];
-    const int key = tid >> 3, part = tid & 7;
-    constexpr int CPT = CPR / 8;   // chunks per thread
-    float a = 0.f, aw = 0.f;
-    u32x4 ch[CPT];
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      ch[i] = *reinterpret_cast<const u32x4*>(&sv[Tile<D>::vidx(key, CPT * part + i)]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) a = dot2(ch[i][e], kOnes, a);
-    }
-    const float vs = group8_sum(a);
-    // the chunk's columns start at an even j, so the pair weights are (1, -1)
-    float vw = 0.f;
-    if constexpr (WCHK) {
-#pragma unroll
-      for (int i = 0; i < CPT; ++i)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) aw = dot2(ch[i][e], kAlt, aw);
-      vw = group8_sum(aw);
-    }
-    if (part == 0) {
-      const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
-      const float hif = __uint_as_float(hi << 16);
-      const uint32_t lo = pack_bf16x2(vs - hif, 0.f) & 0xffffu;
-      svsm[kRowVsHi][key] = (uint16_t)hi;
-      svsm[kRowVsLo][key] = (uint16_t)lo;
-      if constexpr (WCHK) {
-        const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
-        const float whif = __uint_as_float(whi << 16);
-        const uint32_t wlo = pack_bf16x2(vw - whif, 0.f) & 0xffffu;
-        svsm[kRowWHi][key] = (uint16_t)whi;
-        svsm[kRowWLo][key] = (uint16_t)wlo;
-      }
-    }
-    if constexpr (INJECT) {
-      // V site: flip a bit of V[key][col] of this workgroup's copy after
-      // sumrow read it (the thread that owns the chunk writes it back)
-      if (p.f_site == 4 && bh == p.f_bh && qt == p.f_tile && p.f_row - t * BC == key) {
-        const int c = p.f_col >> 3;
-        if (c / CPT == part) {
-#pragma unroll
-          for (int i = 0; i < CPT; ++i)
-            if (CPT * part + i == c) {
-              u32x4 w = ch[i];
-              const int e = (p.f_col & 7) >> 1;
-              const uint32_t mask = (1u << p.f_bit) << (16 * (p.f_col & 1));
-#pragma unroll
-              for (int ee = 0; ee < 4; ++ee)
-                if (ee == e) w[ee] ^= mask;
-              *reinterpret_cast<u32x4*>(&sv[Tile<D>::vidx(key, c)]) = w;
-            }
-        }
-      }
+    if (CHECK && wave == kRecWave) {
+      uint32_t rl = ring_lds;
+      asm volatile("" : "+s"(rl));
+      constexpr uint32_t rOff = offsetof(Ring<D>, vsm) + S * sizeof(Ring<D>::vsm[0]);
+      buffer_load_lds16(rrs, (uint32_t)lane * 16, (uint32_t)t * kRecElems * 2, rl + rOff);
     }
   };
 
@@ -604,18 +565,26 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 
   // ---- pipeline: tiles t+1 and t+2 in flight while tile t is processed
   constexpr int LPT = 2 * NLD;   // loads per thread per tile (K and V)
+  constexpr int LPTR = LPT + 1;  // the same for the wave that loads the record
+  const bool rec_wave = CHECK && wave == kRecWave;
+  // wait until at most n (0, 1 or 2) tiles of this wave's loads are in flight
+  auto wait_tiles = [&](int n) {
+    if (n >= 2) {
+      if (rec_wave) wait_vmcnt<2 * LPTR>();
+      else wait_vmcnt<2 * LPT>();
+    } else if (n == 1) {
+      if (rec_wave) wait_vmcnt<LPTR>();
+      else wait_vmcnt<LPT>();
+    } else {
+      wait_vmcnt<0>();
+    }
+  };
   // tile t sits in stage (t - t_lo) % kStages; the loop below is unrolled
   // kStages times so that each copy knows its stages at compile time
   if (t_end > t_lo) {
     issue(StageId<0>(), t_lo);
     issue(StageId<1>(), t_lo + 1);
     issue(StageId<2>(), t_lo + 2);
-    // first tile complete; the next two may be outstanding
-    if (t_end - t_lo >= 3) wait_vmcnt<2 * LPT>();
-    else if (t_end - t_lo == 2) wait_vmcnt<LPT>();
-    else wait_vmcnt<0>();
-    __syncthreads();
-    if constexpr (CHECK) sumrow(StageId<0>(), t_lo);
   }
   // A use of Q here, on every path into the loop, puts the compiler's own
   // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
@@ -625,18 +594,29 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   static_assert(kStages == 4, "the loop below is unrolled over four stages");
   auto step = [&](auto S_, int t) {
     constexpr int S = decltype(S_)::value;
-    // tile t+1 complete (tile t+2 may still be in flight); after the barrier
-    // every wave is done with tile t-1, whose stage takes tile t+3
-    if (t + 2 < t_end) wait_vmcnt<LPT>();
-    else wait_vmcnt<0>();
+    // tile t complete (tiles t+1 and t+2 may still be in flight); after the
+    // barrier every wave is done with tile t-1, whose stage takes tile t+3
+    wait_tiles(min(2, t_end - 1 - t));
     __syncthreads();
+    if constexpr (INJECT) {
+      // V site: flip a bit of V[row][col] in this workgroup's copy of the
+      // tile, after its sumrow was taken (by vrec_kernel) and before any
+      // wave reads it; the condition is uniform over the workgroup
+      if (p.f_site == 4 && bh == p.f_bh && qt == p.f_tile) {
+        const int key = p.f_row - t * BC;
+        if (key >= 0 && key < BC) {
+          if (tid == 0) {
+            uint16_t* e = ring.v[S] + Tile<D>::vidx(key, p.f_col >> 3) + (p.f_col & 7);
+            *e = (uint16_t)(*e ^ (1u << p.f_bit));
+          }
+          __syncthreads();
+        }
+      }
+    }
     // waves whose rows see none of this tile's keys, or that hold no row
-    // below Lq, skip it (they still load and take sumrow for the others)
+    // below Lq, skip it (they still load for the others)
     if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(S_, t);
     issue(StageId<(S + 3) % kStages>(), t + 3);
-    if constexpr (CHECK) {
-      if (t + 1 < t_end) sumrow(StageId<(S + 1) % kStages>(), t + 1);
-    }
   };
   for (int t = t_lo; t < t_end; t += kStages) {
     step(StageId<0>(), t);
@@ -730,6 +710,65 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       }
     }
   }
+}
+
+// ---- operand records (Eq. 4): sumrow(V)_k = sum_j V_kj and the weighted
+// sum_j (-1)^j V_kj of every key, split into bf16 hi + lo (|x - hi - lo| <=
+// 2^-17 |x|), once per key for all query tiles of the head (the paper's
+// adder shared by the query blocks). One workgroup per (head, key tile),
+// 8 threads per key (fp32 via v_dot2 and a DPP reduction); keys past Lk get 0.
+template <int D>
+__global__ __launch_bounds__(512) void vrec_kernel(const uint16_t* __restrict__ v, int Lk, int ntk,
+                                                   uint16_t* __restrict__ rec) {
+  constexpr int CPT = D / 64;   // 16-byte chunks per thread
+  const int g = blockIdx.x;
+  const int bh = g / ntk, t = g - bh * ntk;
+  const int tid = threadIdx.x, key = tid >> 3, part = tid & 7;
+  const int gk = t * kBc + key;
+  float a = 0.f, aw = 0.f;
+  if (gk < Lk) {
+    const uint16_t* row = v + ((size_t)bh * Lk + gk) * D;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const u32x4 ch = *reinterpret_cast<const u32x4*>(row + 8 * (CPT * part + i));
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a = dot2(ch[e], kOnes, a);
+        // a chunk starts at an even column: pair weights (1, -1)
+        aw = dot2(ch[e], kAlt, aw);
+      }
+    }
+  }
+  const float vs = group8_sum(a), vw = group8_sum(aw);
+  uint16_t* r = rec + (size_t)g * kRecElems;
+  if (part == 0) {
+    const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
+    const uint32_t lo = pack_bf16x2(vs - __uint_as_float(hi << 16), 0.f) & 0xffffu;
+    const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
+    const uint32_t wlo = pack_bf16x2(vw - __uint_as_float(whi << 16), 0.f) & 0xffffu;
+    r[kRowVsHi * kBc + key] = (uint16_t)hi;
+    r[kRowVsLo * kBc + key] = (uint16_t)lo;
+    r[kRowWHi * kBc + key] = (uint16_t)whi;
+    r[kRowWLo * kBc + key] = (uint16_t)wlo;
+  }
+  if (tid < 4 * kBc) {
+    // rows Ones, Zero and the two padding rows
+    const int which = tid / kBc;
+    const int rrow = which == 0 ? kRowOnes : which == 1 ? kRowZero : kRowWLo + which - 1;
+    r[rrow * kBc + (tid % kBc)] = which == 0 ? (uint16_t)0x3f80 : (uint16_t)0;
+  }
+}
+
+int launch_vrec(const uint16_t* v, int BH, int Lk, int d, uint16_t* rec, hipStream_t stream) {
+  const long long ntk = vrec_tiles(Lk);
+  const long long g = (long long)BH * ntk;
+  if (g < 1 || g > INT_MAX) return -1;
+  (void)hipGetLastError();
+  if (d == 128)
+    hipLaunchKernelGGL(vrec_kernel<128>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, rec);
+  else
+    hipLaunchKernelGGL(vrec_kernel<64>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, rec);
+  return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT>

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9):
+    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9, -10):
         assert F.status_str(s) and F.status_str(s) != "unknown status"
     assert F.status_str(12345) == "unknown status"
 
