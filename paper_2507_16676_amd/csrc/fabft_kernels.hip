@@ -715,53 +715,66 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 // ---- operand records (Eq. 4): sumrow(V)_k = sum_j V_kj and the weighted
 // sum_j (-1)^j V_kj of every key, split into bf16 hi + lo (|x - hi - lo| <=
 // 2^-17 |x|), once per key for all query tiles of the head (the paper's
-// adder shared by the query blocks). One workgroup per (head, key tile),
-// 8 threads per key (fp32 via v_dot2 and a DPP reduction); keys past Lk get 0.
+// adder shared by the query blocks). One workgroup per (head, kRecTiles key
+// tiles), 8 threads per key (fp32 via v_dot2 and a DPP reduction); keys past
+// Lk get 0. All of a thread's loads are issued before the first sum.
+constexpr int kRecTiles = 4;
 template <int D>
 __global__ __launch_bounds__(512) void vrec_kernel(const uint16_t* __restrict__ v, int Lk, int ntk,
                                                    uint16_t* __restrict__ rec) {
-  constexpr int CPT = D / 64;   // 16-byte chunks per thread
+  constexpr int CPT = D / 64;   // 16-byte chunks per thread and tile
+  const int nblk = (ntk + kRecTiles - 1) / kRecTiles;
   const int g = blockIdx.x;
-  const int bh = g / ntk, t = g - bh * ntk;
+  const int bh = g / nblk, t0 = (g - bh * nblk) * kRecTiles;
   const int tid = threadIdx.x, key = tid >> 3, part = tid & 7;
-  const int gk = t * kBc + key;
-  float a = 0.f, aw = 0.f;
-  if (gk < Lk) {
-    const uint16_t* row = v + ((size_t)bh * Lk + gk) * D;
+  u32x4 ch[kRecTiles][CPT];
 #pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const u32x4 ch = *reinterpret_cast<const u32x4*>(row + 8 * (CPT * part + i));
+  for (int i = 0; i < kRecTiles; ++i) {
+    const int gk = (t0 + i) * kBc + key;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a = dot2(ch[e], kOnes, a);
-        // a chunk starts at an even column: pair weights (1, -1)
-        aw = dot2(ch[e], kAlt, aw);
-      }
+    for (int c = 0; c < CPT; ++c) {
+      ch[i][c] = u32x4{0, 0, 0, 0};
+      if (t0 + i < ntk && gk < Lk)
+        ch[i][c] = *reinterpret_cast<const u32x4*>(v + ((size_t)bh * Lk + gk) * D +
+                                                   8 * (CPT * part + c));
     }
   }
-  const float vs = group8_sum(a), vw = group8_sum(aw);
-  uint16_t* r = rec + (size_t)g * kRecElems;
-  if (part == 0) {
-    const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
-    const uint32_t lo = pack_bf16x2(vs - __uint_as_float(hi << 16), 0.f) & 0xffffu;
-    const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
-    const uint32_t wlo = pack_bf16x2(vw - __uint_as_float(whi << 16), 0.f) & 0xffffu;
-    r[kRowVsHi * kBc + key] = (uint16_t)hi;
-    r[kRowVsLo * kBc + key] = (uint16_t)lo;
-    r[kRowWHi * kBc + key] = (uint16_t)whi;
-    r[kRowWLo * kBc + key] = (uint16_t)wlo;
-  }
-  if (tid < 4 * kBc) {
-    // rows Ones, Zero and the two padding rows
-    const int which = tid / kBc;
-    const int rrow = which == 0 ? kRowOnes : which == 1 ? kRowZero : kRowWLo + which - 1;
-    r[rrow * kBc + (tid % kBc)] = which == 0 ? (uint16_t)0x3f80 : (uint16_t)0;
+#pragma unroll
+  for (int i = 0; i < kRecTiles; ++i) {
+    if (t0 + i >= ntk) break;   // uniform over the workgroup
+    float a = 0.f, aw = 0.f;
+#pragma unroll
+    for (int c = 0; c < CPT; ++c)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a = dot2(ch[i][c][e], kOnes, a);
+        // a chunk starts at an even column: pair weights (1, -1)
+        aw = dot2(ch[i][c][e], kAlt, aw);
+      }
+    const float vs = group8_sum(a), vw = group8_sum(aw);
+    uint16_t* r = rec + ((size_t)bh * ntk + t0 + i) * kRecElems;
+    if (part == 0) {
+      const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
+      const uint32_t lo = pack_bf16x2(vs - __uint_as_float(hi << 16), 0.f) & 0xffffu;
+      const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
+      const uint32_t wlo = pack_bf16x2(vw - __uint_as_float(whi << 16), 0.f) & 0xffffu;
+      r[kRowVsHi * kBc + key] = (uint16_t)hi;
+      r[kRowVsLo * kBc + key] = (uint16_t)lo;
+      r[kRowWHi * kBc + key] = (uint16_t)whi;
+      r[kRowWLo * kBc + key] = (uint16_t)wlo;
+    }
+    if (tid < 4 * kBc) {
+      // rows Ones, Zero and the two padding rows
+      const int which = tid / kBc;
+      const int rrow = which == 0 ? kRowOnes : which == 1 ? kRowZero : kRowWLo + which - 1;
+      r[rrow * kBc + (tid % kBc)] = which == 0 ? (uint16_t)0x3f80 : (uint16_t)0;
+    }
   }
 }
 
 int launch_vrec(const uint16_t* v, int BH, int Lk, int d, uint16_t* rec, hipStream_t stream) {
   const long long ntk = vrec_tiles(Lk);
-  const long long g = (long long)BH * ntk;
+  const long long g = (long long)BH * ((ntk + kRecTiles - 1) / kRecTiles);
   if (g < 1 || g > INT_MAX) return -1;
   (void)hipGetLastError();
   if (d == 128)
