@@ -208,13 +208,24 @@ enum {
                           sees key k reads the flipped value */
   /* checker state (Section IV-B counts faults there as possible false
      positives): */
-  FABFT_SITE_C = 5,    /* fp32 checksum accumulator c of query row `row`
-                          (its high part) after the update of key tile `tile` */
+  FABFT_SITE_C = 5,    /* fp32 checksum accumulator pair c = c_hi + c_lo of
+                          query row `row` (col 0: c_hi, col 1: c_lo) after
+                          the update of key tile `tile` */
   FABFT_SITE_L = 6,    /* fp32 accumulator l of the row after key tile `tile` */
-  FABFT_SITE_M = 7     /* fp32 running max (scale * log2 e units) of the row,
+  FABFT_SITE_M = 7,    /* fp32 running max (scale * log2 e units) of the row,
                           as held by the lane of the row's first key half,
                           after the exponentials of key tile `tile` */
+  FABFT_SITE_Q = 8,    /* bf16 q_ij in the registers of query row `row`
+                          (col = j), flipped before the Q K^T of key tile
+                          `tile`; the flipped value stays for the later tiles
+                          (a register fault; upstream of o, l and c alike) */
+  FABFT_SITE_VS = 9    /* checker state: the bf16 sumrow(V) operand of key
+                          `row` (col 0: high part, col 1: low part) in the
+                          copy of one workgroup (tile = query tile, as for V) */
 };
+
+/* Most faults one injection launch takes (fabft_attn_fwd_inject_n). */
+#define FABFT_MAX_FAULTS 8
 
 /*
  * One single-bit fault. b, h select the head. For S and P: row = query i,
@@ -223,8 +234,11 @@ enum {
  * a tile that row i processes: t*key_tile <= last visible key of i). For V:
  * row = key k, col = column j, tile = query tile (rows tile*query_tile ..
  * tile*query_tile + query_tile - 1) whose workgroup holds the flipped copy.
- * For C, L, M: row = query i, col = 0, tile as for O.
- * bit: 0..31 for fp32 sites (S, O, C, L, M), 0..15 for bf16 sites (P, V).
+ * For C: row = query i, col 0 or 1, tile as for O. For L, M: row = query i,
+ * col = 0, tile as for O. For Q: row = query i,
+ * col = j < d, tile as for O. For VS: row = key k, col 0 or 1, tile as for V.
+ * bit: 0..31 for fp32 sites (S, O, C, L, M), 0..15 for bf16 sites (P, V, Q,
+ * VS).
  */
 typedef struct {
   int site, b, h, row, col, tile, bit;
@@ -245,6 +259,21 @@ int fabft_attn_fwd_inject(const void* q, const void* k, const void* v,
                           float scale, const fabft_fault* f,
                           float* pred, float* actual,
                           float* pred_w, float* actual_w);
+
+/*
+ * The same with a list of faults applied in one launch (the paper's runs
+ * with several faults): faults[0 .. nfaults-1], each checked as above;
+ * entries with site FABFT_SITE_NONE are skipped. 0 <= nfaults <=
+ * FABFT_MAX_FAULTS (else FABFT_E_FAULT); faults may be NULL when nfaults is
+ * 0. Faults at the same element and time flip that bit once per entry, in
+ * list order.
+ */
+int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v,
+                            void* o, float* resid, uint8_t* flags,
+                            int B, int H, int Lq, int Lk, int d, int causal,
+                            float scale, const fabft_fault* faults, int nfaults,
+                            float* pred, float* actual,
+                            float* pred_w, float* actual_w);
 
 /* Human-readable text for a status code (static storage). */
 const char* fabft_status_str(int status);

@@ -29,9 +29,10 @@ FABFT_OK = 0
 E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE, \
     E_ALLOC = -1, -2, -3, -4, -5, -6, -7, -8, -9, -10
 FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED = 1, 2, 4
-SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M = 0, 1, 2, 3, 4, 5, 6, 7
+SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M, SITE_Q, SITE_VS = range(10)
 SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V,
-         "C": SITE_C, "L": SITE_L, "M": SITE_M}
+         "C": SITE_C, "L": SITE_L, "M": SITE_M, "Q": SITE_Q, "VS": SITE_VS}
+MAX_FAULTS = 8
 
 
 class FabftFault(ctypes.Structure):
@@ -64,6 +65,10 @@ def _load() -> ctypes.CDLL:
     L.fabft_attn_fwd_inject.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                         _f, ctypes.POINTER(FabftFault), _vp, _vp, _vp, _vp]
     L.fabft_attn_fwd_inject.restype = _i
+    L.fabft_attn_fwd_inject_n.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                          _f, ctypes.POINTER(FabftFault), _i, _vp, _vp, _vp,
+                                          _vp]
+    L.fabft_attn_fwd_inject_n.restype = _i
     L.fabft_set_stream.argtypes = [_vp]
     L.fabft_set_stream.restype = None
     L.fabft_set_threshold.argtypes = [_f, _f]
@@ -96,6 +101,7 @@ def _load() -> ctypes.CDLL:
 
 
 EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
+           "fabft_attn_fwd_inject_n",
            "fabft_attn_fwd_splitkv", "fabft_splitkv_workspace_bytes",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
            "fabft_global_check", "fabft_recompute_flagged",
@@ -290,7 +296,7 @@ def global_check(o, resid):
 @dataclass
 class Fault:
     """One single-bit fault for attn_fwd_inject (fields as in fabft_fault)."""
-    site: str          # "S", "P", "O", "V", "C", "L", "M" or "none"
+    site: str          # "S", "P", "O", "V", "C", "L", "M", "Q", "VS" or "none"
     b: int = 0
     h: int = 0
     row: int = 0
@@ -304,9 +310,10 @@ class Fault:
 
 
 def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
-                    fault: Fault | None = None, out=None, weighted_out: bool = False):
-    """Debug / fault-injection forward. Returns (o, resid, flags, pred, actual),
-    followed by (pred_w, actual_w) with weighted_out=True."""
+                    fault=None, out=None, weighted_out: bool = False):
+    """Debug / fault-injection forward. fault: None, one Fault, or a list of
+    up to MAX_FAULTS Faults applied in the same launch. Returns (o, resid,
+    flags, pred, actual), followed by (pred_w, actual_w) with weighted_out=True."""
     import torch
     B, H, Lq, Lk, d = _shape(q, k, v)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
@@ -323,16 +330,16 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
     if weighted_out:
         pw = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
         aw = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
-    f = fault.to_c() if fault is not None else None
+    faults = [] if fault is None else ([fault] if isinstance(fault, Fault) else list(fault))
+    arr = (FabftFault * max(1, len(faults)))(*[f.to_c() for f in faults])
     _stream(dev)
-    _check(_load().fabft_attn_fwd_inject(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                                      resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
-                                      int(bool(causal)), scale,
-                                      ctypes.byref(f) if f is not None else None,
-                                      pred.data_ptr(), actual.data_ptr(),
-                                      pw.data_ptr() if pw is not None else None,
-                                      aw.data_ptr() if aw is not None else None),
-           "fabft_attn_fwd_inject")
+    _check(_load().fabft_attn_fwd_inject_n(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                        resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
+                                        int(bool(causal)), scale, arr, len(faults),
+                                        pred.data_ptr(), actual.data_ptr(),
+                                        pw.data_ptr() if pw is not None else None,
+                                        aw.data_ptr() if aw is not None else None),
+           "fabft_attn_fwd_inject_n")
     if weighted_out:
         return o, resid, flags, pred, actual, pw, aw
     return o, resid, flags, pred, actual
@@ -342,5 +349,5 @@ __all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_splitkv", "splitkv_workspace
            "splitkv_default_splits",
            "global_check", "recompute_flagged", "Fault", "FabftError", "set_threshold",
            "get_threshold", "set_weighted_check", "get_weighted_check", "key_tile",
-           "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "FLAG_RESID",
+           "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "MAX_FAULTS", "FLAG_RESID",
            "FLAG_NONFINITE", "FLAG_WEIGHTED"]

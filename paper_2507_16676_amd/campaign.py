@@ -40,11 +40,30 @@ import time
 import numpy as np
 
 SITES = ("S", "P", "O", "V")
-# checker state (c, l, running max): the paper's false-positive sources
-CHECKER_SITES = ("C", "L", "M")
-SITE_BITS = {"S": 32, "P": 16, "O": 32, "V": 16, "C": 32, "L": 32, "M": 32}
+# checker state (c, l, running max, sumrow record): the paper's false-positive
+# sources
+CHECKER_SITES = ("C", "L", "M", "VS")
+# the storage the paper draws from (Section IV-B): the kernel's per-query
+# registers q, o, m, l and the checker's per-query accumulator c
+PAPER_SITES = ("Q", "O", "M", "L", "C")
+SITE_BITS = {"S": 32, "P": 16, "O": 32, "V": 16, "C": 32, "L": 32, "M": 32, "Q": 16, "VS": 16}
 EXP_BITS = {"S": range(23, 31), "P": range(7, 15), "O": range(23, 31), "V": range(7, 15),
-            "C": range(23, 31), "L": range(23, 31), "M": range(23, 31)}
+            "C": range(23, 31), "L": range(23, 31), "M": range(23, 31), "Q": range(7, 15),
+            "VS": range(7, 15)}
+
+
+def storage_bits(w, site):
+    """Bits one query row keeps in `site` for the whole pass: q (d bf16), the
+    output accumulator o (d fp32), m and l (fp32 each) and c (an fp32 pair,
+    c_hi + c_lo: 64 bits, like the paper's double-precision accumulator)."""
+    return {"Q": 16 * w.d, "O": 32 * w.d, "M": 32, "L": 32, "C": 64}[site]
+
+
+def storage_weights(w, sites):
+    """Probability of each site when a flipped bit is drawn uniformly over
+    the storage of all sites (each row holds the same storage)."""
+    bits = np.array([storage_bits(w, s) for s in sites], dtype=np.float64)
+    return bits / bits.sum()
 SIG_REL = 2.0 ** -8
 
 
@@ -77,31 +96,59 @@ def device_inputs(w, seed, device="cuda"):
             v.to(torch.bfloat16).contiguous())
 
 
-def draw_fault(run: int, w, key_tile: int, query_tile: int, sites=SITES):
+def draw_fault(run: int, w, key_tile: int, query_tile: int, sites=SITES, weights=None):
     """The fault of run `run`: site, head, element and bit, uniform over live
-    elements (visible keys for S/P, processed key tiles for O, query tiles
-    that can see the key for V)."""
-    from . import Fault
+    elements (visible keys for S/P, processed key tiles for O/Q/C/L/M, query
+    tiles that can see the key for V/VS). Sites are equally likely, or drawn
+    with probabilities `weights`."""
+    return _draw_one(np.random.default_rng(int(run)), w, key_tile, query_tile, sites, weights)
+
+
+def draw_faults(run: int, w, key_tile: int, query_tile: int, sites=SITES, weights=None,
+                kmin=1, kmax=1):
+    """The faults of run `run`: k in [kmin, kmax] drawn uniformly, then k
+    independent faults as in draw_fault, all in the head of the first one
+    (the campaign recomputes one head per run). With kmin = kmax = 1 this is
+    [draw_fault(run, ...)]."""
     rng = np.random.default_rng(int(run))
-    site = sites[int(rng.integers(len(sites)))]
+    if kmin == kmax == 1:
+        return [_draw_one(rng, w, key_tile, query_tile, sites, weights)]
+    k = int(rng.integers(kmin, kmax + 1))
+    out = []
+    for i in range(k):
+        f = _draw_one(rng, w, key_tile, query_tile, sites, weights)
+        if i:
+            f = type(f)(f.site, out[0].b, out[0].h, f.row, f.col, f.tile, f.bit)
+        out.append(f)
+    return out
+
+
+def _draw_one(rng, w, key_tile, query_tile, sites, weights):
+    from . import Fault
+    if weights is None:
+        site = sites[int(rng.integers(len(sites)))]
+    else:
+        site = sites[int(rng.choice(len(sites), p=np.asarray(weights, dtype=np.float64)))]
     b = int(rng.integers(w.B))
     h = int(rng.integers(w.H))
     off = w.Lk - w.Lq
     bit = int(rng.integers(SITE_BITS[site]))
-    if site in ("S", "P", "O", "C", "L", "M"):
+    if site in ("S", "P", "O", "C", "L", "M", "Q"):
         while True:
             row = int(rng.integers(w.Lq))
             last = min(w.Lk - 1, row + off) if w.causal else w.Lk - 1
             if last >= 0:
                 break
-        if site in ("O", "C", "L", "M"):
-            col = int(rng.integers(w.d)) if site == "O" else 0
+        if site in ("O", "C", "L", "M", "Q"):
+            col = (int(rng.integers(w.d)) if site in ("O", "Q") else
+                   int(rng.integers(2)) if site == "C" else 0)
             tile = int(rng.integers(last // key_tile + 1))
         else:
             col = int(rng.integers(last + 1))
             tile = 0
         return Fault(site, b, h, row, col, tile, bit)
-    # V: key k, column j, one query tile whose rows can see key k
+    # V, VS: key k, column j (V) or part (VS), one query tile whose rows can
+    # see key k
     n_qt = (w.Lq + query_tile - 1) // query_tile
     while True:
         key = int(rng.integers(w.Lk))
@@ -112,9 +159,9 @@ def draw_fault(run: int, w, key_tile: int, query_tile: int, sites=SITES):
                 continue
             first = max(0, lo_row) // query_tile
         break
-    col = int(rng.integers(w.d))
+    col = int(rng.integers(w.d)) if site == "V" else int(rng.integers(2))
     tile = int(rng.integers(first, n_qt))
-    return Fault("V", b, h, key, col, tile, bit)
+    return Fault(site, b, h, key, col, tile, bit)
 
 
 def classify(o, o_gold, flags):
@@ -141,10 +188,11 @@ def classify(o, o_gold, flags):
             "nonfinite": bool(nonfinite_rows.any())}
 
 
-def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES):
+def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES, weights=None,
+                 kmin=1, kmax=1):
     """Run faults start..runs-1 on workload w (inputs drawn with `seed`),
     appending one JSON line per run to out_path; runs already in the file
-    are skipped."""
+    are skipped. Each run injects k in [kmin, kmax] faults (draw_faults)."""
     torch = _torch()
     from . import attn_fwd_inject, global_check, key_tile, query_tile
     done = set()
@@ -164,7 +212,8 @@ def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES
         for r in range(start, runs):
             if r in done:
                 continue
-            f = draw_fault(r, w, bc, qt, sites)
+            fl = draw_faults(r, w, bc, qt, sites, weights, kmin, kmax)
+            f = fl[0]
             b, h = f.b, f.h
             qh, kh, vh = q[b:b + 1, h:h + 1], k[b:b + 1, h:h + 1], v[b:b + 1, h:h + 1]
             if (b, h) not in gold:
@@ -172,16 +221,18 @@ def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES
                 torch.cuda.synchronize()
                 assert int(fg.sum()) == 0, f"fault-free head ({b},{h}) flagged"
                 gold[(b, h)] = og
-            f_local = type(f)(f.site, 0, 0, f.row, f.col, f.tile, f.bit)
+            f_local = [type(x)(x.site, 0, 0, x.row, x.col, x.tile, x.bit) for x in fl]
             o, resid, flags, pred, actual = attn_fwd_inject(qh, kh, vh, causal=w.causal,
                                                             scale=w.scale, fault=f_local)
             res = classify(o[0, 0], gold[(b, h)][0, 0], flags[0, 0])
             # the paper's single check per attention, on the same output
             _, gflag = global_check(o, resid)
-            rec = {"run": r, "site": f.site, "b": b, "h": h, "row": f.row, "col": f.col,
-                   "tile": f.tile, "bit": f.bit,
-                   "exponent_bit": f.bit in EXP_BITS[f.site], **res,
-                   "global_flag": int(gflag[0, 0])}
+            rec = {"run": r, "site": f.site if len(fl) == 1 else "multi", "b": b, "h": h,
+                   "row": f.row, "col": f.col, "tile": f.tile, "bit": f.bit,
+                   "exponent_bit": any(x.bit in EXP_BITS[x.site] for x in fl),
+                   "nfaults": len(fl), **res, "global_flag": int(gflag[0, 0])}
+            if len(fl) > 1:
+                rec["faults"] = [[x.site, x.row, x.col, x.tile, x.bit] for x in fl]
             out.write(json.dumps(rec) + "\n")
             n_new += 1
             if log_every and n_new % log_every == 0:
@@ -223,7 +274,7 @@ def summarize(path):
             gl["detected" if r["global_flag"] else "silent"] += 1
     ng = gl["detected"] + gl["silent"]
     per_site = {}
-    for s in SITES + CHECKER_SITES:
+    for s in SITES + CHECKER_SITES + ("Q", "multi"):
         if ("all", s) not in table:
             continue
         t = table.get(("all", s), {})
@@ -231,7 +282,25 @@ def summarize(path):
         per_site[s] = {**t, "runs": tot,
                        "raw_detect_rate": (t.get("detected", 0) / tot) if tot else None}
     per_bit = {f"{s}{b}": table[("bit", s, b)] for (_, s, b) in
-               sorted(k for k in table if k[0] == "bit")}
+               sorted(k for k in table if k[0] == "bit") if s != "multi"}
+
+    # the paper's three classes (Table I): every run that changed something
+    # or raised a flag is Detected (flagged, output changed), False positive
+    # (flagged, output bitwise unchanged) or Silent (significant error, not
+    # flagged); runs that changed the output only below the significance
+    # level without a flag, or nothing at all, are counted apart as benign
+    def paper_table(rs):
+        c = {"detected": 0, "false_positive": 0, "silent": 0, "benign": 0}
+        for r in rs:
+            o = r["outcome"]
+            c["detected" if o in ("detected", "detected_minor") else o] += 1
+        nb = c["detected"] + c["false_positive"] + c["silent"]
+        pct = {k: (100.0 * c[k] / nb if nb else float("nan"))
+               for k in ("detected", "false_positive", "silent")}
+        return {"runs": len(rs), **c, "pct_of_non_benign": pct}
+    by_k = {}
+    for r in recs:
+        by_k.setdefault(int(r.get("nfaults", 1)), []).append(r)
     return {"runs": len(recs),
             "headline": {"what": "exponent-bit flips at P, O, V: detected / (detected + silent)",
                          "detected": head["detected"], "silent": head["silent"],
@@ -244,7 +313,9 @@ def summarize(path):
             "global_false_alarms": sum(1 for r in recs if r.get("global_flag")
                                        and r["outcome"] in ("false_positive", "benign")),
             "false_positives": sum(1 for r in recs if r["outcome"] == "false_positive"),
-            "per_site": per_site, "per_bit": per_bit}
+            "per_site": per_site, "per_bit": per_bit,
+            "paper_table": paper_table(recs),
+            "paper_table_by_nfaults": {k: paper_table(v) for k, v in sorted(by_k.items())}}
 
 
 def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000):
@@ -309,8 +380,14 @@ def main(argv=None):
     c.add_argument("--summary")
     c.add_argument("--weighted", action="store_true",
                    help="also run the weighted (alternating-sign) checksum")
-    c.add_argument("--sites", default="S,P,O,V",
-                   help="comma-separated fault sites to draw from (S,P,O,V,C,L,M)")
+    c.add_argument("--sites", default=None,
+                   help="comma-separated fault sites to draw from (S,P,O,V,C,L,M,Q,VS); "
+                        "default S,P,O,V, or Q,O,M,L,C with --storage-weighted")
+    c.add_argument("--storage-weighted", action="store_true",
+                   help="draw sites with probability proportional to their storage bits "
+                        "(sites Q,O,M,L,C: the paper's per-query registers)")
+    c.add_argument("--faults", default="1",
+                   help="faults per run: K or KMIN-KMAX (drawn uniformly; one head per run)")
     s = sub.add_parser("sweep")
     s.add_argument("--workload", default="dec_l4096")
     s.add_argument("--seeds", type=int, default=10000)
@@ -325,15 +402,25 @@ def main(argv=None):
         from . import set_weighted_check
         set_weighted_check(True)
     if a.cmd == "campaign":
-        summ = run_campaign(w, a.runs, a.out, seed=a.seed, start=a.start,
-                            sites=tuple(a.sites.split(",")))
+        sites = tuple(a.sites.split(",")) if a.sites else (
+            PAPER_SITES if a.storage_weighted else SITES)
+        weights = storage_weights(w, sites) if a.storage_weighted else None
+        kmin, _, kmax = a.faults.partition("-")
+        kmin = int(kmin)
+        kmax = int(kmax) if kmax else kmin
+        summ = run_campaign(w, a.runs, a.out, seed=a.seed, start=a.start, sites=sites,
+                            weights=weights, kmin=kmin, kmax=kmax)
+        summ["sites"] = list(sites)
+        summ["site_weights"] = None if weights is None else [float(x) for x in weights]
+        summ["faults_per_run"] = [kmin, kmax]
         summ["weighted_check"] = bool(a.weighted)
         txt = json.dumps(summ, indent=1)
         if a.summary:
             with open(a.summary, "w") as f:
                 f.write(txt)
         print(json.dumps({"runs": summ["runs"], "headline": summ["headline"],
-                          "false_positives": summ["false_positives"]}))
+                          "false_positives": summ["false_positives"],
+                          "paper_table": summ["paper_table"]}))
     else:
         print(json.dumps(run_sweep(w, a.seeds, a.out, seed0=a.seed0, rho_every=a.rho_every)))
 

@@ -11,6 +11,8 @@
 #include "../../include/fabft.h"
 #include "fabft_kernels.h"
 
+static_assert(FABFT_MAX_FAULTS == fabft::kMaxFaults, "fault list size");
+
 namespace {
 
 hipStream_t g_stream = nullptr;
@@ -78,8 +80,8 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.sl2 = scale * kLog2e;
   p.tau_rel = g_tau_rel;
   p.tau_abs = g_tau_abs;
-  p.f_site = 0;
-  p.f_bh = p.f_row = p.f_col = p.f_tile = p.f_bit = -1;
+  p.nf = 0;
+  for (int i = 0; i < fabft::kMaxFaults; ++i) p.f[i] = fabft::FaultDesc{0, -1, -1, -1, -1, -1};
   return p;
 }
 
@@ -153,58 +155,86 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
                 causal, 0, B * H);
 }
 
-int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,
-                          uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
-                          float scale, const fabft_fault* f, float* pred, float* actual,
-                          float* pred_w, float* actual_w) {
+}  // extern "C"
+
+namespace {
+
+// Range checks of one fault descriptor against the problem (site semantics in
+// include/fabft.h).
+int check_fault(const fabft_fault* f, int B, int H, int Lq, int Lk, int d, int causal, int n_qt) {
+  if (f->b < 0 || f->b >= B || f->h < 0 || f->h >= H) return FABFT_E_FAULT;
+  const int off = Lk - Lq;
+  const int bc = fabft::key_tile(d);
+  switch (f->site) {
+    case FABFT_SITE_S:
+    case FABFT_SITE_P:
+      if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= Lk) return FABFT_E_FAULT;
+      if (causal && f->col > f->row + off) return FABFT_E_FAULT;
+      if (f->bit < 0 || f->bit >= (f->site == FABFT_SITE_S ? 32 : 16)) return FABFT_E_FAULT;
+      return FABFT_OK;
+    case FABFT_SITE_C:
+    case FABFT_SITE_L:
+    case FABFT_SITE_M:
+    case FABFT_SITE_O:
+    case FABFT_SITE_Q: {
+      const int ncol = (f->site == FABFT_SITE_O || f->site == FABFT_SITE_Q) ? d
+                       : f->site == FABFT_SITE_C                            ? 2
+                                                                             : 1;
+      if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= ncol) return FABFT_E_FAULT;
+      if (f->bit < 0 || f->bit >= (f->site == FABFT_SITE_Q ? 16 : 32)) return FABFT_E_FAULT;
+      const long long last = causal ? std::min<long long>(Lk - 1, (long long)f->row + off)
+                                    : (long long)Lk - 1;
+      if (last < 0 || f->tile < 0 || (long long)f->tile * bc > last) return FABFT_E_FAULT;
+      return FABFT_OK;
+    }
+    case FABFT_SITE_V:
+    case FABFT_SITE_VS:
+      if (f->row < 0 || f->row >= Lk || f->col < 0 ||
+          f->col >= (f->site == FABFT_SITE_V ? d : 2))
+        return FABFT_E_FAULT;
+      if (f->tile < 0 || f->tile >= n_qt) return FABFT_E_FAULT;
+      if (f->bit < 0 || f->bit >= 16) return FABFT_E_FAULT;
+      return FABFT_OK;
+    default:
+      return FABFT_E_FAULT;
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o, float* resid,
+                            uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                            float scale, const fabft_fault* faults, int nfaults, float* pred,
+                            float* actual, float* pred_w, float* actual_w) {
   int n_qt = 0, grid = 0;
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   if (!resid || !flags) return FABFT_E_NULL;
+  if (nfaults < 0 || nfaults > FABFT_MAX_FAULTS) return FABFT_E_FAULT;
+  if (nfaults > 0 && !faults) return FABFT_E_NULL;
   fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid);
   p.pred = pred;
   p.actual = actual;
   p.pred_w = pred_w;
   p.actual_w = actual_w;
-  if (f && f->site != FABFT_SITE_NONE) {
-    if (f->b < 0 || f->b >= B || f->h < 0 || f->h >= H) return FABFT_E_FAULT;
-    const int off = Lk - Lq;
-    const int bc = fabft::key_tile(d);
-    switch (f->site) {
-      case FABFT_SITE_S:
-      case FABFT_SITE_P:
-        if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= Lk) return FABFT_E_FAULT;
-        if (causal && f->col > f->row + off) return FABFT_E_FAULT;
-        if (f->bit < 0 || f->bit >= (f->site == FABFT_SITE_S ? 32 : 16)) return FABFT_E_FAULT;
-        break;
-      case FABFT_SITE_C:
-      case FABFT_SITE_L:
-      case FABFT_SITE_M:
-      case FABFT_SITE_O: {
-        const int ncol = f->site == FABFT_SITE_O ? d : 1;
-        if (f->row < 0 || f->row >= Lq || f->col < 0 || f->col >= ncol) return FABFT_E_FAULT;
-        if (f->bit < 0 || f->bit >= 32) return FABFT_E_FAULT;
-        const long long last = causal ? std::min<long long>(Lk - 1, (long long)f->row + off)
-                                      : (long long)Lk - 1;
-        if (last < 0 || f->tile < 0 || (long long)f->tile * bc > last) return FABFT_E_FAULT;
-        break;
-      }
-      case FABFT_SITE_V:
-        if (f->row < 0 || f->row >= Lk || f->col < 0 || f->col >= d) return FABFT_E_FAULT;
-        if (f->tile < 0 || f->tile >= n_qt) return FABFT_E_FAULT;
-        if (f->bit < 0 || f->bit >= 16) return FABFT_E_FAULT;
-        break;
-      default:
-        return FABFT_E_FAULT;
-    }
-    p.f_site = f->site;
-    p.f_bh = f->b * H + f->h;
-    p.f_row = f->row;
-    p.f_col = f->col;
-    p.f_tile = f->tile;
-    p.f_bit = f->bit;
+  for (int i = 0; i < nfaults; ++i) {
+    const fabft_fault* f = faults + i;
+    if (f->site == FABFT_SITE_NONE) continue;
+    rc = check_fault(f, B, H, Lq, Lk, d, causal, n_qt);
+    if (rc != FABFT_OK) return rc;
+    p.f[p.nf++] = fabft::FaultDesc{f->site, f->b * H + f->h, f->row, f->col, f->tile, f->bit};
   }
   return launch(p, d, causal, 2, B * H);
+}
+
+int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,
+                          uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                          float scale, const fabft_fault* f, float* pred, float* actual,
+                          float* pred_w, float* actual_w) {
+  return fabft_attn_fwd_inject_n(q, k, v, o, resid, flags, B, H, Lq, Lk, d, causal, scale, f,
+                                 f ? 1 : 0, pred, actual, pred_w, actual_w);
 }
 
 void fabft_set_stream(void* hip_stream) { g_stream = static_cast<hipStream_t>(hip_stream); }

@@ -18,6 +18,13 @@ inline long long vrec_bytes(long long BH, int Lk) {
   return BH * vrec_tiles(Lk) * kRecElems * 2;
 }
 
+// One injected single-bit fault (site numbers and fields as fabft_fault,
+// with the head flattened to bh = b * H + h).
+constexpr int kMaxFaults = 8;
+struct FaultDesc {
+  int site, bh, row, col, tile, bit;
+};
+
 struct FwdParams {
   const uint16_t* q;
   const uint16_t* k;
@@ -43,7 +50,8 @@ struct FwdParams {
   int grid;       // workgroups = B * H * n_qt
   float sl2;      // scale * log2(e)
   float tau_rel, tau_abs;
-  int f_site, f_bh, f_row, f_col, f_tile, f_bit;  // fault (site 0 = none)
+  int nf;                          // faults in f (injection kernels only)
+  FaultDesc f[kMaxFaults];
 };
 
 // mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection,

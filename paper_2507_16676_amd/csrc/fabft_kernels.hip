@@ -372,6 +372,24 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     const int kv0 = t * BC;
     const bool need_mask = (kv0 + BC > Lk) || (CAUSAL && kv0 + BC - 1 > wq_lo + off);
 
+    if constexpr (INJECT) {
+      // Q site: bit of q_ij in the registers of row i, flipped before the
+      // Q K^T of tile f_tile; the flipped value stays for the later tiles
+      // (lane grp holds columns 16s + 8grp .. +7 of its row)
+      for (int fi = 0; fi < p.nf; ++fi) {
+        const FaultDesc fd = p.f[fi];
+        if (fd.site == 8 && bh == fd.bh && qrow == fd.row && t == fd.tile &&
+            ((fd.col >> 3) & 1) == grp) {
+          const int sj = fd.col >> 4, e = (fd.col & 7) >> 1;
+          const uint32_t mask = (1u << fd.bit) << (16 * (fd.col & 1));
+#pragma unroll
+          for (int s2 = 0; s2 < NDS; ++s2)
+#pragma unroll
+            for (int ee = 0; ee < 4; ++ee)
+              if (s2 == sj && ee == e) qf[s2][ee] ^= mask;
+        }
+      }
+    }
     // S^T = K Q^T (Alg. 3: s_i = q . k_i)
     f32x16 sacc[NKB];
 #pragma unroll
@@ -396,16 +414,19 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     __builtin_amdgcn_sched_barrier(0);
     // accumulator element i of block kb holds key kv0 + 32kb + 16(i/8) + 8grp + (i%8)
     if constexpr (INJECT) {
-      if (p.f_site == 1 && bh == p.f_bh && qrow == p.f_row) {
-        const int kl = p.f_col - kv0;
-        if (kl >= 0 && kl < BC && ((kl >> 3) & 1) == grp) {
-          const int kb = kl >> 5, i = ((kl >> 4) & 1) * 8 + (kl & 7);
+      for (int fi = 0; fi < p.nf; ++fi) {
+        const FaultDesc fd = p.f[fi];
+        if (fd.site == 1 && bh == fd.bh && qrow == fd.row) {
+          const int kl = fd.col - kv0;
+          if (kl >= 0 && kl < BC && ((kl >> 3) & 1) == grp) {
+            const int kb = kl >> 5, i = ((kl >> 4) & 1) * 8 + (kl & 7);
 #pragma unroll
-          for (int b = 0; b < NKB; ++b)
+            for (int b = 0; b < NKB; ++b)
 #pragma unroll
-            for (int e = 0; e < 16; ++e)
-              if (b == kb && e == i)
-                sacc[b][e] = __uint_as_float(__float_as_uint(sacc[b][e]) ^ (1u << p.f_bit));
+              for (int e = 0; e < 16; ++e)
+                if (b == kb && e == i)
+                  sacc[b][e] = __uint_as_float(__float_as_uint(sacc[b][e]) ^ (1u << fd.bit));
+          }
         }
       }
     }
@@ -463,8 +484,11 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     if constexpr (INJECT) {
       // M site (checker state): the running max of the lane holding the
       // row's first key half, after this tile's exponentials
-      if (p.f_site == 7 && bh == p.f_bh && qrow == p.f_row && t == p.f_tile && grp == 0)
-        m2_run = __uint_as_float(__float_as_uint(m2_run) ^ (1u << p.f_bit));
+      for (int fi = 0; fi < p.nf; ++fi) {
+        const FaultDesc fd = p.f[fi];
+        if (fd.site == 7 && bh == fd.bh && qrow == fd.row && t == fd.tile && grp == 0)
+          m2_run = __uint_as_float(__float_as_uint(m2_run) ^ (1u << fd.bit));
+      }
     }
 
     // c = c*alpha + sumrow(V) p~ and l = l*alpha + sum p~ (Alg. 3): the
@@ -485,22 +509,27 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
         aux = mfma32(a, pb[kb][h], aux);
       }
     if constexpr (INJECT) {
-      // C and L sites (checker state): the fp32 accumulator c (its high
-      // part) or l of the row after this tile's update
-      if ((p.f_site == 5 || p.f_site == 6) && bh == p.f_bh && qrow == p.f_row &&
-          t == p.f_tile && grp == 0) {
-        const int el = p.f_site == 5 ? 0 : 2;
+      // C and L sites (checker state): a part of the fp32 accumulator pair
+      // c = c_hi + c_lo, or l, of the row after this tile's update
+      for (int fi = 0; fi < p.nf; ++fi) {
+        const FaultDesc fd = p.f[fi];
+        if ((fd.site == 5 || fd.site == 6) && bh == fd.bh && qrow == fd.row && t == fd.tile &&
+            grp == 0) {
+          const int el = fd.site == 5 ? fd.col : 2;   // c: hi (0) or lo (1) part
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if (i == el) aux[i] = __uint_as_float(__float_as_uint(aux[i]) ^ (1u << p.f_bit));
+          for (int i = 0; i < 16; ++i)
+            if (i == el) aux[i] = __uint_as_float(__float_as_uint(aux[i]) ^ (1u << fd.bit));
+        }
       }
     }
     if constexpr (INJECT) {
-      if (p.f_site == 2 && bh == p.f_bh && qrow == p.f_row) {
-        const int kl = p.f_col - kv0;
+      for (int fi = 0; fi < p.nf; ++fi) {
+        const FaultDesc fd = p.f[fi];
+        if (!(fd.site == 2 && bh == fd.bh && qrow == fd.row)) continue;
+        const int kl = fd.col - kv0;
         if (kl >= 0 && kl < BC && ((kl >> 3) & 1) == grp) {
           const int kb = kl >> 5, h = (kl >> 4) & 1, e = (kl & 7) >> 1;
-          const uint32_t mask = (1u << p.f_bit) << (16 * (kl & 1));
+          const uint32_t mask = (1u << fd.bit) << (16 * (kl & 1));
 #pragma unroll
           for (int b = 0; b < NKB; ++b)
 #pragma unroll
@@ -547,8 +576,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (INJECT) {
       // O site: accumulator element (row, col) after the P V of tile f_tile
-      if (p.f_site == 3 && bh == p.f_bh && qrow == p.f_row && t == p.f_tile) {
-        const int j = p.f_col;
+      for (int fi = 0; fi < p.nf; ++fi) {
+        const FaultDesc fd = p.f[fi];
+        if (!(fd.site == 3 && bh == fd.bh && qrow == fd.row && t == fd.tile)) continue;
+        const int j = fd.col;
         // output column j = 32db + 8a + 4grp + (i%4), element i = 4a + (i%4)
         if (((j >> 2) & 1) == grp) {
           const int db = j >> 5, i = 4 * ((j >> 3) & 3) + (j & 3);
@@ -557,7 +588,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
             for (int e = 0; e < 16; ++e)
               if (b == db && e == i)
-                oacc[b][e] = __uint_as_float(__float_as_uint(oacc[b][e]) ^ (1u << p.f_bit));
+                oacc[b][e] = __uint_as_float(__float_as_uint(oacc[b][e]) ^ (1u << fd.bit));
         }
       }
     }
@@ -602,16 +633,25 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       // V site: flip a bit of V[row][col] in this workgroup's copy of the
       // tile, after its sumrow was taken (by vrec_kernel) and before any
       // wave reads it; the condition is uniform over the workgroup
-      if (p.f_site == 4 && bh == p.f_bh && qt == p.f_tile) {
-        const int key = p.f_row - t * BC;
-        if (key >= 0 && key < BC) {
-          if (tid == 0) {
-            uint16_t* e = ring.v[S] + Tile<D>::vidx(key, p.f_col >> 3) + (p.f_col & 7);
-            *e = (uint16_t)(*e ^ (1u << p.f_bit));
+      // VS site (checker state): the same for the tile's sumrow record
+      // (col 0: hi part, col 1: lo part); faults apply one after another
+      bool hit = false;
+      for (int fi = 0; fi < p.nf; ++fi) {
+        const FaultDesc fd = p.f[fi];
+        if ((fd.site == 4 || fd.site == 9) && bh == fd.bh && qt == fd.tile) {
+          const int key = fd.row - t * BC;
+          if (key >= 0 && key < BC) {
+            hit = true;
+            if (tid == 0) {
+              uint16_t* e = fd.site == 4
+                                ? ring.v[S] + Tile<D>::vidx(key, fd.col >> 3) + (fd.col & 7)
+                                : &ring.vsm[S][kRowVsHi + fd.col][key];
+              *e = (uint16_t)(*e ^ (1u << fd.bit));
+            }
           }
-          __syncthreads();
         }
       }
+      if (hit) __syncthreads();
     }
     // waves whose rows see none of this tile's keys, or that hold no row
     // below Lq, skip it (they still load for the others)

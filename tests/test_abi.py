@@ -100,10 +100,18 @@ def test_nocheck_rejects_bad_arguments():
     F.Fault("V", row=8, col=0, tile=0),           # key >= Lk
     F.Fault("V", row=0, col=0, tile=1),           # only one query tile
     F.Fault("V", row=0, col=0, tile=0, bit=16),
-    F.Fault("C", row=0, col=1, tile=0),           # checker sites have one column
+    F.Fault("C", row=0, col=2, tile=0),           # c has two parts (hi, lo)
+    F.Fault("L", row=0, col=1, tile=0),           # l and m have one column
     F.Fault("L", row=8, col=0, tile=0),           # row >= Lq
     F.Fault("M", row=3, col=0, tile=1),           # tile past the row's keys
     F.Fault("C", row=0, col=0, tile=0, bit=32),
+    F.Fault("Q", row=3, col=128, tile=0),         # col >= d
+    F.Fault("Q", row=3, col=0, tile=0, bit=16),   # q is bf16
+    F.Fault("Q", row=3, col=0, tile=1),           # tile past the row's keys
+    F.Fault("VS", row=0, col=2, tile=0),          # two parts (hi, lo)
+    F.Fault("VS", row=8, col=0, tile=0),          # key >= Lk
+    F.Fault("VS", row=0, col=0, tile=1),          # only one query tile
+    F.Fault("VS", row=0, col=1, tile=0, bit=16),
 ])
 def test_inject_rejects_bad_faults(fault):
     f = fault.to_c()
@@ -113,10 +121,26 @@ def test_inject_rejects_bad_faults(fault):
 
 
 def test_inject_rejects_unknown_site():
-    f = F.FabftFault(9, 0, 0, 0, 0, 0, 0)
-    rc = F.lib().fabft_attn_fwd_inject(P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 0.1,
-                                       ctypes.byref(f), None, None, None, None)
-    assert rc == F.E_FAULT
+    for site in (10, 99, -1):
+        f = F.FabftFault(site, 0, 0, 0, 0, 0, 0)
+        rc = F.lib().fabft_attn_fwd_inject(P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 0.1,
+                                           ctypes.byref(f), None, None, None, None)
+        assert rc == F.E_FAULT
+
+
+def test_inject_n_validates_the_list():
+    L = F.lib()
+    args = (P, P, P, P, P, P, 1, 2, 8, 8, 128, 1, 0.1)
+    good = F.Fault("O", row=3, col=0, tile=0).to_c()
+    bad = F.Fault("O", row=3, col=0, tile=1).to_c()
+    arr = (F.FabftFault * 9)(*([good] * 9))
+    assert L.fabft_attn_fwd_inject_n(*args, arr, F.MAX_FAULTS + 1, None, None, None, None) \
+        == F.E_FAULT
+    assert L.fabft_attn_fwd_inject_n(*args, arr, -1, None, None, None, None) == F.E_FAULT
+    assert L.fabft_attn_fwd_inject_n(*args, None, 2, None, None, None, None) == F.E_NULL
+    # one bad entry anywhere in the list rejects the call before any launch
+    arr2 = (F.FabftFault * 3)(good, good, bad)
+    assert L.fabft_attn_fwd_inject_n(*args, arr2, 3, None, None, None, None) == F.E_FAULT
 
 
 def test_global_check_validation():

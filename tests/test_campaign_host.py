@@ -20,13 +20,16 @@ def _valid(f, w, bc, qt):
         assert 0 <= f.row < w.Lq and 0 <= f.col < w.Lk
         assert not w.causal or f.col <= f.row + off
         assert 0 <= f.bit < (32 if f.site == "S" else 16)
-    elif f.site in ("O", "C", "L", "M"):
-        ncol = w.d if f.site == "O" else 1
-        assert 0 <= f.row < w.Lq and 0 <= f.col < ncol and 0 <= f.bit < 32
+    elif f.site in ("O", "C", "L", "M", "Q"):
+        ncol = w.d if f.site in ("O", "Q") else 2 if f.site == "C" else 1
+        assert 0 <= f.row < w.Lq and 0 <= f.col < ncol
+        assert 0 <= f.bit < (16 if f.site == "Q" else 32)
         last = min(w.Lk - 1, f.row + off) if w.causal else w.Lk - 1
         assert 0 <= f.tile * bc <= last
     else:
-        assert 0 <= f.row < w.Lk and 0 <= f.col < w.d and 0 <= f.bit < 16
+        assert f.site in ("V", "VS")
+        assert 0 <= f.row < w.Lk and 0 <= f.col < (w.d if f.site == "V" else 2)
+        assert 0 <= f.bit < 16
         n_qt = (w.Lq + qt - 1) // qt
         assert 0 <= f.tile < n_qt
         # some row of the query tile sees the key
@@ -112,3 +115,45 @@ def test_summary_counts(tmp_path):
     assert s["false_positives"] == 1
     assert s["per_site"]["S"]["silent"] == 1
     assert s["per_bit"]["O30"]["detected"] == 1
+
+
+def test_storage_weights_follow_the_register_sizes():
+    w = W.WORKLOADS["dec_l4096"]   # d = 128
+    p = C.storage_weights(w, C.PAPER_SITES)
+    bits = dict(zip(C.PAPER_SITES, p * (16 * 128 + 32 * 128 + 32 + 32 + 64)))
+    assert bits == pytest.approx({"Q": 2048, "O": 4096, "M": 32, "L": 32, "C": 64})
+    assert p.sum() == pytest.approx(1.0)
+    # the checker's share shrinks as d grows (the paper's trend in Table I)
+    w64 = W.Workload("d64", 1, 1, 256, 256, 64, False, 0.125)
+    assert C.storage_weights(w64, C.PAPER_SITES)[-1] > p[-1]
+
+
+def test_storage_weighted_draws_match_the_weights():
+    w = W.Workload("t1", 1, 4, 256, 256, 64, True, 0.125)
+    p = C.storage_weights(w, C.PAPER_SITES)
+    n = 20000
+    counts = {s: 0 for s in C.PAPER_SITES}
+    for r in range(n):
+        f = C.draw_fault(r, w, 64, 256, C.PAPER_SITES, p)
+        _valid(f, w, 64, 256)
+        counts[f.site] += 1
+    for s, pi in zip(C.PAPER_SITES, p):
+        sd = (n * pi * (1 - pi)) ** 0.5
+        assert abs(counts[s] - n * pi) <= 5 * sd + 1, (s, counts[s], n * pi)
+
+
+def test_multi_fault_draws_share_a_head_and_are_reproducible():
+    w = W.Workload("t1", 2, 4, 256, 256, 128, True, 0.125)
+    p = C.storage_weights(w, C.PAPER_SITES)
+    ks = set()
+    for r in range(500):
+        fl = C.draw_faults(r, w, 64, 256, C.PAPER_SITES, p, 1, 5)
+        assert 1 <= len(fl) <= 5
+        ks.add(len(fl))
+        assert len({(f.b, f.h) for f in fl}) == 1
+        for f in fl:
+            _valid(f, w, 64, 256)
+        assert fl == C.draw_faults(r, w, 64, 256, C.PAPER_SITES, p, 1, 5)
+    assert ks == {1, 2, 3, 4, 5}
+    # one fault per run reproduces the single-fault draw
+    assert C.draw_faults(7, w, 64, 256) == [C.draw_fault(7, w, 64, 256)]

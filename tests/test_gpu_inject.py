@@ -152,3 +152,46 @@ def test_m_site_flip_stays_in_its_row(golden):
     others = flags.clone()
     others[0, 1, 290] = 0
     assert int(others.sum()) == 0
+
+
+def test_q_site_is_upstream_of_the_checksum(golden):
+    """A q register fault changes every later score of its row; o, l and c
+    all use the resulting p~, so the row's output moves but its checksum
+    still matches (the paper's check cannot see it)."""
+    (_, (o0, r0, f0, p0, a0)) = golden
+    f = F.Fault("Q", b=0, h=1, row=250, col=37, tile=1, bit=10)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    assert _changed_rows(o, o0) == {(0, 1, 250)}
+    assert int(flags.sum()) == 0
+    tau, _ = F.get_threshold()
+    O = G.from_dev_bf16(o)[0, 1, 250]
+    M = np.abs(O).sum() + abs(float(pred[0, 1, 250]))
+    assert abs(float(resid[0, 1, 250])) <= tau * M
+
+
+def test_vs_site_is_a_false_positive(golden):
+    """A flip in the sumrow record of one workgroup changes pred of its rows
+    that weight the key, not O: an alarm with a correct result."""
+    (_, (o0, r0, f0, p0, a0)) = golden
+    qt = F.query_tile()
+    f = F.Fault("VS", b=0, h=1, row=100, col=0, tile=1, bit=14)
+    o, resid, flags, pred, actual = _inject(golden, f)
+    assert torch.equal(o.view(torch.int16), o0.view(torch.int16))
+    assert torch.equal(actual, a0)
+    flagged = set(map(tuple, (flags != 0).nonzero().cpu().numpy().tolist()))
+    assert flagged and flagged <= {(0, 1, i) for i in range(qt, W_INJ.Lq)}
+
+
+def test_several_faults_in_one_launch(golden):
+    (_, (o0, r0, f0, p0, a0)) = golden
+    faults = [F.Fault("O", b=0, h=0, row=40, col=3, tile=0, bit=30),
+              F.Fault("O", b=0, h=1, row=270, col=100, tile=2, bit=30),
+              F.Fault("P", b=0, h=1, row=10, col=5, bit=14)]
+    o, resid, flags, pred, actual = _inject(golden, faults)
+    assert _changed_rows(o, o0) == {(0, 0, 40), (0, 1, 270), (0, 1, 10)}
+    for b, h, i in ((0, 0, 40), (0, 1, 270), (0, 1, 10)):
+        assert int(flags[b, h, i]) != 0, (b, h, i)
+    # an empty list is the fault-free debug run
+    o2, r2, f2, _, _ = _inject(golden, [])
+    assert torch.equal(o2.view(torch.int16), o0.view(torch.int16))
+    assert torch.equal(r2.view(torch.int32), r0.view(torch.int32))

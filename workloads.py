@@ -112,6 +112,12 @@ WORKLOADS = {
                           1.0 / math.sqrt(128.0)),
     "long_l32768": Workload("long_l32768", 1, 32, 32768, 32768, 128, True,
                             1.0 / math.sqrt(128.0), peaked_frac=0.01),
+    # the fault-detection setting of Table I (one attention layer, sequence
+    # length 256): an encoder head shape with d = 64 (non-causal) and a
+    # decoder head shape with d = 128 (causal); synthetic stand-ins
+    "t1_enc_d64": Workload("t1_enc_d64", 1, 12, 256, 256, 64, False, 1.0 / 8.0),
+    "t1_dec_d128": Workload("t1_dec_d128", 1, 32, 256, 256, 128, True,
+                            1.0 / math.sqrt(128.0)),
 }
 
 
