@@ -27,7 +27,9 @@
  *    entry point allocates nothing. Besides that buffer the library keeps a
  *    stream, the detection threshold and the weighted-check switch as
  *    process-global state (not thread-safe).
- *  - d must be 64 or 128. B, H, Lq, Lk >= 1. scale must be finite and >= 0.
+ *  - d must be 64, 96 or 128 (d = 96 runs the d = 128 kernels with the
+ *    columns 96..127 zero on chip: identical results, 4/3 of the work).
+ *    B, H, Lq, Lk >= 1. scale must be finite and >= 0.
  *  - causal != 0 keeps key k for query i iff k <= i + (Lk - Lq)
  *    (bottom-right aligned; the plain lower triangle when Lq == Lk). A query
  *    row with no visible key gets O = 0, pred = actual = resid = 0, flag 0.
@@ -55,7 +57,7 @@ enum {
   FABFT_E_NULL = -1,     /* a required pointer is NULL */
   FABFT_E_SHAPE = -2,    /* B, H, Lq or Lk < 1, or the grid is too large, or
                             (Lk + 64) * d * 2 >= 2^32 */
-  FABFT_E_HEADDIM = -3,  /* d is not 64 or 128 */
+  FABFT_E_HEADDIM = -3,  /* d is not 64, 96 or 128 */
   FABFT_E_ALIGN = -4,    /* q, k, v or o not 16-byte aligned */
   FABFT_E_LAUNCH = -5,   /* the kernel launch failed */
   FABFT_E_SCALE = -6,    /* scale negative, NaN or infinite */

@@ -35,11 +35,12 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int validate(const void* q, const void* k, const void* v, void* o, int B, int H, int Lq,
              int Lk, int d, float scale, int* n_qt, int* grid) {
   if (!q || !k || !v || !o) return FABFT_E_NULL;
-  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
   if (B < 1 || H < 1 || Lq < 1 || Lk < 1) return FABFT_E_SHAPE;
-  // K and V of one head are addressed with 32-bit byte offsets (one key tile
-  // of slack for the last tile's reads)
-  if ((static_cast<long long>(Lk) + 64) * d * 2 > 0xffffffffLL) return FABFT_E_SHAPE;
+  // K and V of one head are addressed with 32-bit byte offsets; reads past
+  // the end (the last tile, padding columns at d = 96) sit up to one more
+  // head size further, which must not wrap either
+  if ((static_cast<long long>(Lk) + 64) * d * 4 > 0xffffffffLL) return FABFT_E_SHAPE;
   // one operand record per (head, key tile), indexed in 32 bits
   if (static_cast<long long>(B) * H * fabft::vrec_tiles(Lk) > INT_MAX) return FABFT_E_SHAPE;
   if (!std::isfinite(scale) || scale < 0.f) return FABFT_E_SCALE;
@@ -54,9 +55,10 @@ int validate(const void* q, const void* k, const void* v, void* o, int B, int H,
 }
 
 fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* o,
-                             float* resid, uint8_t* flags, int Lq, int Lk, float scale,
+                             float* resid, uint8_t* flags, int Lq, int Lk, int d, float scale,
                              int n_qt, int grid) {
   fabft::FwdParams p{};
+  p.dio = d;
   p.q = static_cast<const uint16_t*>(q);
   p.k = static_cast<const uint16_t*>(k);
   p.v = static_cast<const uint16_t*>(v);
@@ -142,7 +144,7 @@ int fabft_attn_fwd(const void* q, const void* k, const void* v, void* o, float* 
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   if (!resid || !flags) return FABFT_E_NULL;
-  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid), d, causal, 1,
+  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid), d, causal, 1,
                 B * H);
 }
 
@@ -151,7 +153,7 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
   int n_qt = 0, grid = 0;
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
-  return launch(make_params(q, k, v, o, nullptr, nullptr, Lq, Lk, scale, n_qt, grid), d,
+  return launch(make_params(q, k, v, o, nullptr, nullptr, Lq, Lk, d, scale, n_qt, grid), d,
                 causal, 0, B * H);
 }
 
@@ -214,7 +216,7 @@ int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o
   if (!resid || !flags) return FABFT_E_NULL;
   if (nfaults < 0 || nfaults > FABFT_MAX_FAULTS) return FABFT_E_FAULT;
   if (nfaults > 0 && !faults) return FABFT_E_NULL;
-  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid);
+  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid);
   p.pred = pred;
   p.actual = actual;
   p.pred_w = pred_w;
@@ -252,9 +254,11 @@ void fabft_get_threshold(float* tau_rel, float* tau_abs) {
 }
 
 long long fabft_splitkv_workspace_bytes(int B, int H, int Lq, int d, int nsplit) {
-  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
   if (B < 1 || H < 1 || Lq < 1 || nsplit < 1 || nsplit > kMaxSplits) return FABFT_E_SHAPE;
-  return static_cast<long long>(B) * H * Lq * nsplit * fabft::split_record_floats(d) *
+  // partial outputs are kept at the kernels' compute width
+  return static_cast<long long>(B) * H * Lq * nsplit *
+         fabft::split_record_floats(fabft::compute_width(d)) *
          static_cast<long long>(sizeof(float));
 }
 
@@ -272,7 +276,7 @@ int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v, void* o,
   if (workspace_bytes < need) return FABFT_E_WORKSPACE;
   const long long g = static_cast<long long>(grid) * nsplit;
   if (g > INT_MAX) return FABFT_E_SHAPE;
-  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, scale, n_qt, grid);
+  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid);
   const int bc = fabft::key_tile(d);
   const int tiles = (Lk + bc - 1) / bc;
   p.nsplit = nsplit;
@@ -320,7 +324,7 @@ int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o
       int n_qt1 = 0, grid1 = 0;
       rc = validate(qh, kh, vh, oh, 1, 1, Lq, Lk, d, scale, &n_qt1, &grid1);
       if (rc != FABFT_OK) return rc;
-      rc = launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, scale, n_qt1, grid1), d, causal, 1, 1);
+      rc = launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, d, scale, n_qt1, grid1), d, causal, 1, 1);
       if (rc != FABFT_OK) return rc;
       if (fabft::launch_head_flags(fh, 1, Lq, head_flags + bh, g_stream) != 0) return FABFT_E_LAUNCH;
       if (hipMemcpyAsync(head_flags_host + bh, head_flags + bh, 1, hipMemcpyDeviceToHost,
@@ -338,7 +342,7 @@ int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o
 int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq, int d,
                        double* gsum, uint8_t* gflags) {
   if (!o || !resid || !gsum || !gflags) return FABFT_E_NULL;
-  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
   if (B < 1 || H < 1 || Lq < 1) return FABFT_E_SHAPE;
   if (static_cast<long long>(B) * H > INT_MAX) return FABFT_E_SHAPE;
   if (!aligned16(o)) return FABFT_E_ALIGN;
@@ -352,7 +356,7 @@ void fabft_set_weighted_check(int on) { g_wcheck = on ? 1 : 0; }
 int fabft_get_weighted_check(void) { return g_wcheck; }
 
 int fabft_key_tile(int d) {
-  if (d != 64 && d != 128) return FABFT_E_HEADDIM;
+  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
   return fabft::key_tile(d);
 }
 
@@ -363,7 +367,7 @@ const char* fabft_status_str(int status) {
     case FABFT_OK: return "ok";
     case FABFT_E_NULL: return "null pointer argument";
     case FABFT_E_SHAPE: return "invalid shape (B, H, Lq, Lk must be >= 1; grid too large)";
-    case FABFT_E_HEADDIM: return "unsupported head dimension (d must be 64 or 128)";
+    case FABFT_E_HEADDIM: return "unsupported head dimension (d must be 64, 96 or 128)";
     case FABFT_E_ALIGN: return "q, k, v and o must be 16-byte aligned";
     case FABFT_E_LAUNCH: return "kernel launch failed";
     case FABFT_E_SCALE: return "scale must be finite and >= 0";

@@ -43,6 +43,8 @@ struct FwdParams {
   int nsplit;
   int split_tiles;
   float* ws;
+  int dio;               // head dimension of q, k, v, o in memory (<= the
+                         // kernel's width; the rest of the width is zero)
   const uint16_t* vrec;  // operand records of every head (checked modes)
   int ntk;               // key tiles per head in vrec
   int Lq, Lk;
@@ -60,6 +62,9 @@ int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t str
 int key_tile(int d);
 // sumrow(V) records of BH heads (Eq. 4) into rec (vrec_bytes(BH, Lk) bytes).
 int launch_vrec(const uint16_t* v, int BH, int Lk, int d, uint16_t* rec, hipStream_t stream);
+// Width the kernels compute with for a head dimension d (64, 96 or 128): d
+// itself, or 128 for d = 96 (columns 96..127 are zero on chip).
+inline int compute_width(int d) { return d == 96 ? 128 : d; }
 // Partial-state record of (head, row, split) in the split workspace, in
 // floats: m (exp2 domain), l, c, c_w, then the d unnormalised outputs o.
 inline int split_record_floats(int d) { return d + 4; }

@@ -271,8 +271,12 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   const int Lq = p.Lq, Lk = p.Lk;
   const int q0 = qt * kBr;
   const int off = Lk - Lq;
-  const size_t qbase = (size_t)bh * (size_t)Lq * D;
-  const size_t kbase = (size_t)bh * (size_t)Lk * D;
+  // q, k, v, o rows hold DIO <= D columns in memory; on chip the rows are D
+  // wide and columns DIO.. are zero (zero scores, zero outputs)
+  const int DIO = p.dio;
+  const int CIO = DIO / 8;   // 16-byte chunks per row in memory
+  const size_t qbase = (size_t)bh * (size_t)Lq * DIO;
+  const size_t kbase = (size_t)bh * (size_t)Lk * DIO;
 
   int kend = Lk;
   if (CAUSAL) kend = min(Lk, q0 + kBr + off);
@@ -293,8 +297,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
   for (int s = 0; s < NDS; ++s) {
     qf[s] = u32x4{0, 0, 0, 0};
-    if (qrow < Lq)
-      qf[s] = *reinterpret_cast<const u32x4*>(p.q + qbase + (size_t)qrow * D + 16 * s + 8 * grp);
+    if (qrow < Lq && 2 * s + grp < CIO)
+      qf[s] = *reinterpret_cast<const u32x4*>(p.q + qbase + (size_t)qrow * DIO + 16 * s + 8 * grp);
   }
 
   f32x16 oacc[NDB];
@@ -322,8 +326,9 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
   // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk read as
   // zeros (the mask gives them weight 0)
-  const i32x4 krs = buffer_rsrc(p.k + kbase, (uint32_t)Lk * D * 2);
-  const i32x4 vrs = buffer_rsrc(p.v + kbase, (uint32_t)Lk * D * 2);
+  const uint32_t kv_bytes = (uint32_t)Lk * DIO * 2;
+  const i32x4 krs = buffer_rsrc(p.k + kbase, kv_bytes);
+  const i32x4 vrs = buffer_rsrc(p.v + kbase, kv_bytes);
   // the operand record of each key tile (1 KiB) is loaded by one wave
   constexpr int kRecWave = kWaves - 1;
   const i32x4 rrs = buffer_rsrc(CHECK ? p.vrec + (size_t)bh * p.ntk * kRecElems : p.v,
@@ -333,8 +338,11 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   for (int j = 0; j < NLD; ++j) {
     const int slot = j * kThreads + tid;
     const int row = slot / CPR, sc = slot % CPR;
-    kvo[j] = (uint32_t)(row * D + 8 * (sc ^ Tile<D>::kswz(row))) * 2;
-    vvo[j] = (uint32_t)(row * D + 8 * (sc ^ Tile<D>::vswz(row))) * 2;
+    // a chunk past the row's DIO columns reads from offset kv_bytes + soff,
+    // past the end of the buffer: zeros
+    const int kc = sc ^ Tile<D>::kswz(row), vc = sc ^ Tile<D>::vswz(row);
+    kvo[j] = kc < CIO ? (uint32_t)(row * DIO + 8 * kc) * 2 : kv_bytes;
+    vvo[j] = vc < CIO ? (uint32_t)(row * DIO + 8 * vc) * 2 : kv_bytes;
   }
   // LDS byte address of the ring and of this wave's 1 KiB slot in a tile
   const uint32_t ring_lds = (uint32_t)(uintptr_t)(lds_void*)&ring;
@@ -342,7 +350,7 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   auto issue = [&](auto S_, int t) {
     constexpr int S = decltype(S_)::value;
     if (t >= t_end) return;
-    const uint32_t soff = (uint32_t)t * BC * D * 2;
+    const uint32_t soff = (uint32_t)t * BC * DIO * 2;
     // opaque copy: the destination addresses are formed here from one SGPR
     // (scalar adds) rather than hoisted as one live SGPR per stage and load
     uint32_t wl = wave_lds;
@@ -704,15 +712,17 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       act_w += (i & 1) ? -x : x;
     }
   if (qrow < Lq) {
-    uint16_t* orow = p.o + qbase + (size_t)qrow * D;
+    uint16_t* orow = p.o + qbase + (size_t)qrow * DIO;
 #pragma unroll
-    for (int db = 0; db < NDB; ++db)
+    for (int db = 0; db < NDB; ++db) {
+      if (32 * db >= DIO) break;   // DIO is a multiple of 32
 #pragma unroll
       for (int a = 0; a < 4; ++a) {
         const u32x2 w = {pack_bf16x2(oacc[db][4 * a], oacc[db][4 * a + 1]),
                          pack_bf16x2(oacc[db][4 * a + 2], oacc[db][4 * a + 3])};
         *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * a + 4 * grp) = w;
       }
+    }
   }
   if constexpr (CHECK) {
     act = sum_xor32(act);
@@ -761,8 +771,8 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
 constexpr int kRecTiles = 4;
 template <int D>
 __global__ __launch_bounds__(512) void vrec_kernel(const uint16_t* __restrict__ v, int Lk, int ntk,
-                                                   uint16_t* __restrict__ rec) {
-  constexpr int CPT = D / 64;   // 16-byte chunks per thread and tile
+                                                   int dio, uint16_t* __restrict__ rec) {
+  constexpr int CPT = D / 64;   // 16-byte chunks per thread and tile (rows D wide)
   const int nblk = (ntk + kRecTiles - 1) / kRecTiles;
   const int g = blockIdx.x;
   const int bh = g / nblk, t0 = (g - bh * nblk) * kRecTiles;
@@ -774,8 +784,8 @@ __global__ __launch_bounds__(512) void vrec_kernel(const uint16_t* __restrict__ 
 #pragma unroll
     for (int c = 0; c < CPT; ++c) {
       ch[i][c] = u32x4{0, 0, 0, 0};
-      if (t0 + i < ntk && gk < Lk)
-        ch[i][c] = *reinterpret_cast<const u32x4*>(v + ((size_t)bh * Lk + gk) * D +
+      if (t0 + i < ntk && gk < Lk && 8 * (CPT * part + c) < dio)
+        ch[i][c] = *reinterpret_cast<const u32x4*>(v + ((size_t)bh * Lk + gk) * dio +
                                                    8 * (CPT * part + c));
     }
   }
@@ -817,10 +827,12 @@ int launch_vrec(const uint16_t* v, int BH, int Lk, int d, uint16_t* rec, hipStre
   const long long g = (long long)BH * ((ntk + kRecTiles - 1) / kRecTiles);
   if (g < 1 || g > INT_MAX) return -1;
   (void)hipGetLastError();
-  if (d == 128)
-    hipLaunchKernelGGL(vrec_kernel<128>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, rec);
+  if (compute_width(d) == 128)
+    hipLaunchKernelGGL(vrec_kernel<128>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, d,
+                       rec);
   else
-    hipLaunchKernelGGL(vrec_kernel<64>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, rec);
+    hipLaunchKernelGGL(vrec_kernel<64>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, d,
+                       rec);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -902,14 +914,14 @@ __global__ __launch_bounds__(64 * kMergeWaves) void merge_kernel(FwdParams p, in
   }
   const float inv = l > 0.f ? 1.0f / l : 0.f;
   float act = 0.f, absum = 0.f, act_w = 0.f;
-  uint16_t* orow = p.o + ((size_t)bh * rows_per_head + row) * D;
+  uint16_t* orow = p.o + ((size_t)bh * rows_per_head + row) * p.dio;
 #pragma unroll
   for (int u = 0; u < CPL; ++u) {
-    const float x = o[u] * inv;
+    const float x = o[u] * inv;   // 0 for columns past dio
     act += x;
     absum += __builtin_fabsf(x);
     act_w += (lane & 1) ? -x : x;   // column lane + 64u has the parity of lane
-    orow[lane + 64 * u] = (uint16_t)(pack_bf16x2(x, 0.f) & 0xffffu);
+    if (lane + 64 * u < p.dio) orow[lane + 64 * u] = (uint16_t)(pack_bf16x2(x, 0.f) & 0xffffu);
   }
   act = wave_sum(act);
   absum = wave_sum(absum);
@@ -939,7 +951,7 @@ int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream) {
   if (g > INT_MAX) return -1;
   (void)hipGetLastError();
   const dim3 grid((unsigned)g), block(64 * kMergeWaves);
-  if (d == 128) {
+  if (compute_width(d) == 128) {
     if (p.wcheck) hipLaunchKernelGGL((merge_kernel<128, true>), grid, block, 0, stream, p, p.Lq);
     else hipLaunchKernelGGL((merge_kernel<128, false>), grid, block, 0, stream, p, p.Lq);
   } else {
@@ -950,11 +962,11 @@ int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream) {
 }
 
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream) {
-  if (d == 128) return launch_d<128>(p, causal, mode, stream);
+  if (compute_width(d) == 128) return launch_d<128>(p, causal, mode, stream);
   return launch_d<64>(p, causal, mode, stream);
 }
 
-int key_tile(int d) { return (d == 64 || d == 128) ? kBc : 0; }
+int key_tile(int d) { return (d == 64 || d == 96 || d == 128) ? kBc : 0; }
 
 // ---- global check of one head (Alg. 3, the check accumulated over all
 // queries; Eq. 5 in its per-query form, Eq. 6-7): R = sum_i (pred_i -
@@ -973,7 +985,7 @@ __global__ __launch_bounds__(kGThreads) void global_check_kernel(
   const uint16_t* ob = o + (size_t)bh * Lq * d;
   double sr = 0.0, sa = 0.0;
   for (int i = tid; i < Lq; i += kGThreads) sr += (double)r[i];
-  // O as 8-element chunks (rows are 16-byte aligned: d is 64 or 128)
+  // O as 8-element chunks (rows are 16-byte aligned: d is 64, 96 or 128)
   const size_t nchunk = (size_t)Lq * d / 8;
   for (size_t c = tid; c < nchunk; c += kGThreads) {
     const u32x4 w = *reinterpret_cast<const u32x4*>(ob + 8 * c);

@@ -41,8 +41,9 @@ def test_key_and_query_tiles():
     assert F.key_tile(128) == 64
     assert F.key_tile(64) == 64
     assert F.query_tile() == 256
+    assert F.key_tile(96) == 64
     with pytest.raises(F.FabftError):
-        F.key_tile(96)
+        F.key_tile(80)
 
 
 def test_threshold_validation_and_roundtrip():
@@ -63,7 +64,7 @@ def test_threshold_validation_and_roundtrip():
     ((0, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
     ((P, P, P, P, 0, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
     ((P, P, P, P, P, 0, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
-    ((P, P, P, P, P, P, 1, 1, 8, 8, 96, 0, 1.0), F.E_HEADDIM),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 80, 0, 1.0), F.E_HEADDIM),
     ((P, P, P, P, P, P, 1, 1, 8, 8, 256, 0, 1.0), F.E_HEADDIM),
     ((P, P, P, P, P, P, 0, 1, 8, 8, 128, 0, 1.0), F.E_SHAPE),
     ((P, P, P, P, P, P, 1, 0, 8, 8, 128, 0, 1.0), F.E_SHAPE),
@@ -147,7 +148,7 @@ def test_global_check_validation():
     L = F.lib()
     assert L.fabft_global_check(None, P, 1, 1, 8, 128, P, P) == F.E_NULL
     assert L.fabft_global_check(P, P, 1, 1, 8, 128, None, P) == F.E_NULL
-    assert L.fabft_global_check(P, P, 1, 1, 8, 96, P, P) == F.E_HEADDIM
+    assert L.fabft_global_check(P, P, 1, 1, 8, 80, P, P) == F.E_HEADDIM
     assert L.fabft_global_check(P, P, 0, 1, 8, 128, P, P) == F.E_SHAPE
     assert L.fabft_global_check(P, P, 1, 1, 0, 128, P, P) == F.E_SHAPE
     assert L.fabft_global_check(P + 2, P, 1, 1, 8, 128, P, P) == F.E_ALIGN
@@ -157,7 +158,9 @@ def test_splitkv_workspace_size_and_validation():
     L = F.lib()
     assert L.fabft_splitkv_workspace_bytes(2, 3, 5, 128, 4) == 2 * 3 * 5 * 4 * (128 + 4) * 4
     assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 64, 1) == (64 + 4) * 4
-    assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 96, 1) == F.E_HEADDIM
+    assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 80, 1) == F.E_HEADDIM
+    # d = 96 keeps its partial outputs at the compute width 128
+    assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 96, 1) == (128 + 4) * 4
     assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 128, 0) == F.E_SHAPE
     assert L.fabft_splitkv_workspace_bytes(1, 1, 1, 128, 65) == F.E_SHAPE
     need = L.fabft_splitkv_workspace_bytes(1, 2, 8, 128, 4)
@@ -178,7 +181,7 @@ def test_recompute_flagged_validation():
     assert L.fabft_recompute_flagged(*base, None, P, 2, *ok[3:]) == F.E_NULL
     assert L.fabft_recompute_flagged(*base, P, None, 2, *ok[3:]) == F.E_NULL
     assert L.fabft_recompute_flagged(*base, P, P, 2, None, ctypes.byref(n2)) == F.E_NULL
-    bad_d = base[:10] + (96,) + base[11:]
+    bad_d = base[:10] + (80,) + base[11:]
     assert L.fabft_recompute_flagged(*bad_d, *ok) == F.E_HEADDIM
     no_flags = base[:5] + (None,) + base[6:]
     assert L.fabft_recompute_flagged(*no_flags, *ok) == F.E_NULL

@@ -195,3 +195,34 @@ def test_several_faults_in_one_launch(golden):
     o2, r2, f2, _, _ = _inject(golden, [])
     assert torch.equal(o2.view(torch.int16), o0.view(torch.int16))
     assert torch.equal(r2.view(torch.int32), r0.view(torch.int32))
+
+
+def test_d96_faults_on_the_last_columns():
+    """d = 96 runs the d = 128 kernel with zero columns 96..127 on chip: an
+    O fault in column 95 and a V fault in column 90 behave as at d = 128,
+    and nothing is written past column 95."""
+    w = W.Workload("inj96", 1, 2, 300, 300, 96, True, 96 ** -0.5, seed=9)
+    q, k, v = G.dev_inputs(W.make_inputs(w))
+    o0, r0, f0, p0, a0 = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale)
+    torch.cuda.synchronize()
+    assert int(f0.sum()) == 0
+    f = F.Fault("O", b=0, h=1, row=200, col=95, tile=2, bit=30)
+    o, resid, flags, pred, actual = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale,
+                                                      fault=f)
+    torch.cuda.synchronize()
+    assert _changed_rows(o, o0) == {(0, 1, 200)} and int(flags[0, 1, 200]) != 0
+    f = F.Fault("V", b=0, h=0, row=40, col=90, tile=0, bit=14)
+    o, resid, flags, pred, actual = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale,
+                                                      fault=f)
+    torch.cuda.synchronize()
+    changed = _changed_rows(o, o0)
+    assert changed and all(h == 0 and i >= 40 for _, h, i in changed)
+    assert int(flags[0, 0].sum()) != 0
+    # the output buffer holds exactly [B, H, L, 96]: a guard band after it
+    # stays untouched
+    buf = torch.full((o0.numel() + 64,), -7, dtype=torch.int16, device=q.device)
+    ob = buf[:o0.numel()].view(torch.bfloat16).view(o0.shape)
+    F.attn_fwd(q, k, v, causal=True, scale=w.scale, out=(ob, r0.clone(), f0.clone()))
+    torch.cuda.synchronize()
+    assert torch.all(buf[o0.numel():] == -7)
+    assert torch.equal(ob.view(torch.int16), o0.view(torch.int16))

@@ -21,6 +21,7 @@ CASES = [
     (W.Workload("dec7c64", 2, 2, 7, 777, 64, True, 0.125, seed=13), 20),   # 13 tiles: empty splits
     (W.Workload("sq300", 1, 2, 300, 300, 128, True, 128 ** -0.5, seed=14), 3),
     (W.Workload("one", 1, 1, 5, 2000, 64, False, 0.125, seed=15), 1),
+    (W.Workload("dec3d96", 2, 2, 3, 1500, 96, True, 96 ** -0.5, seed=16), 6),
 ]
 
 

@@ -116,6 +116,7 @@ WORKLOADS = {
     # length 256): an encoder head shape with d = 64 (non-causal) and a
     # decoder head shape with d = 128 (causal); synthetic stand-ins
     "t1_enc_d64": Workload("t1_enc_d64", 1, 12, 256, 256, 64, False, 1.0 / 8.0),
+    "t1_dec_d96": Workload("t1_dec_d96", 1, 32, 256, 256, 96, True, 1.0 / math.sqrt(96.0)),
     "t1_dec_d128": Workload("t1_dec_d128", 1, 32, 256, 256, 128, True,
                             1.0 / math.sqrt(128.0)),
 }
