@@ -230,9 +230,8 @@ def main():
     log(f"[bench] checksum off: {ms_off:.4f} ms/step, {tflops_off:.1f} TFLOP/s; "
         f"interleaved on {ms_on_r:.4f} ms/step; overhead {overhead:.2f}%")
 
-    # ---- roofline of the checksum-on step: the forward kernel and the sumrow
-    # pre-pass it needs (one HIP-event interval per step covers both; the
-    # forward is ~97% of it)
+    # ---- roofline of the dominant kernel (the checksum-on forward; one
+    # launch per step)
     achieved = flops / (avg_launch_ms * 1e-3) / 1e12
     traffic = None
     tf = TRAFFIC_FILE.format(workload=w.name)
@@ -244,8 +243,8 @@ def main():
     roofline = {"bound": "mfma", "achieved": round(achieved, 2),
                 "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
-                "kernel": (f"fabft::vrec_kernel<{w.d}> + fabft::fwd_kernel<{w.d}, "
-                           f"{str(w.causal).lower()}, true, false, false, false> (one step)"),
+                "kernel": (f"fabft::fwd_kernel<{w.d}, {str(w.causal).lower()}, true, false, "
+                           f"false, false>"),
                 "avg_launch_ms": round(avg_launch_ms, 5)}
 
     if args.copy_probe_mib > 0:

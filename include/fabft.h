@@ -17,17 +17,10 @@
  *    contiguous row-major [B, H, Lq, d] (q, o) and [B, H, Lk, d] (k, v),
  *    16-byte aligned. resid is fp32 [B, H, Lq], flags is uint8 [B, H, Lq],
  *    pred/actual (when given) fp32 [B, H, Lq]; all device pointers.
- *  - The caller owns every buffer it passes. The checked entry points also
- *    need sumrow(V) of every key (Eq. 4): a pre-pass kernel on the library
- *    stream writes it, once per key for all query rows, into a device buffer
- *    of B * H * ceil(Lk / 64) KiB that the library allocates on the current
- *    device on first use and replaces by a larger one when a call needs more
- *    (that replacement synchronises the device); it is kept until the
- *    process ends (FABFT_E_ALLOC if the allocation fails). The unchecked
- *    entry point allocates nothing. Besides that buffer the library keeps a
- *    stream, the detection threshold and the weighted-check switch as
- *    process-global state (not thread-safe).
- *  - d must be 64, 96 or 128 (d = 96 runs the d = 128 kernels with the
+ *  - The caller owns every buffer. The library allocates nothing and keeps
+ *    only a stream, the detection threshold and the weighted-check switch as
+ *    process-global state (setters are not thread-safe).
+ *  - d must be 64, 96, 128 or 256 (d = 96 runs the d = 128 kernels with the
  *    columns 96..127 zero on chip: identical results, 4/3 of the work).
  *    B, H, Lq, Lk >= 1. scale must be finite and >= 0.
  *  - causal != 0 keeps key k for query i iff k <= i + (Lk - Lq)
@@ -57,14 +50,13 @@ enum {
   FABFT_E_NULL = -1,     /* a required pointer is NULL */
   FABFT_E_SHAPE = -2,    /* B, H, Lq or Lk < 1, or the grid is too large, or
                             (Lk + 64) * d * 2 >= 2^32 */
-  FABFT_E_HEADDIM = -3,  /* d is not 64, 96 or 128 */
+  FABFT_E_HEADDIM = -3,  /* d is not 64, 96, 128 or 256 */
   FABFT_E_ALIGN = -4,    /* q, k, v or o not 16-byte aligned */
   FABFT_E_LAUNCH = -5,   /* the kernel launch failed */
   FABFT_E_SCALE = -6,    /* scale negative, NaN or infinite */
   FABFT_E_FAULT = -7,    /* fault descriptor out of range */
   FABFT_E_THRESHOLD = -8, /* threshold negative or NaN */
-  FABFT_E_WORKSPACE = -9, /* workspace smaller than fabft_splitkv_workspace_bytes */
-  FABFT_E_ALLOC = -10     /* the library's sumrow buffer could not be allocated */
+  FABFT_E_WORKSPACE = -9  /* workspace smaller than fabft_splitkv_workspace_bytes */
 };
 
 /* Detection flags, one byte per query row. */
@@ -146,8 +138,7 @@ void fabft_get_threshold(float* tau_rel, float* tau_abs);
  * head still flagged after max_retries is counted as persistent (its O is
  * not trusted). Counts go to *n_recovered and *n_persistent.
  * head_flags: device buffer of B*H bytes; head_flags_host: host buffer of
- * B*H bytes (both caller-owned; besides them only the sumrow buffer of the
- * checked forward is used).
+ * B*H bytes (both caller-owned scratch; the library allocates nothing).
  * Unlike the other entry points this one synchronises the library stream
  * (it needs the flags on the host). max_retries >= 1.
  */
@@ -192,9 +183,10 @@ int fabft_get_weighted_check(void);
  * of fabft_fault.tile at the O site), or FABFT_E_HEADDIM. */
 int fabft_key_tile(int d);
 
-/* Number of query rows per workgroup (the unit of fabft_fault.tile at the
- * V site). */
-int fabft_query_tile(void);
+/* Number of query rows per workgroup for head dimension d (the unit of
+ * fabft_fault.tile at the V and VS sites): 256, or 128 at d = 256;
+ * FABFT_E_HEADDIM for an unsupported d. */
+int fabft_query_tile(int d);
 
 /* Fault sites for the injection path (where a single bit is flipped). */
 enum {

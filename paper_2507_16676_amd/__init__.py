@@ -26,8 +26,8 @@ _vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
 _fp = ctypes.POINTER(ctypes.c_float)
 
 FABFT_OK = 0
-E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE, \
-    E_ALLOC = -1, -2, -3, -4, -5, -6, -7, -8, -9, -10
+E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE = \
+    -1, -2, -3, -4, -5, -6, -7, -8, -9
 FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED = 1, 2, 4
 SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M, SITE_Q, SITE_VS = range(10)
 SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V,
@@ -92,7 +92,7 @@ def _load() -> ctypes.CDLL:
     L.fabft_get_weighted_check.restype = _i
     L.fabft_key_tile.argtypes = [_i]
     L.fabft_key_tile.restype = _i
-    L.fabft_query_tile.argtypes = []
+    L.fabft_query_tile.argtypes = [_i]
     L.fabft_query_tile.restype = _i
     L.fabft_status_str.argtypes = [_i]
     L.fabft_status_str.restype = ctypes.c_char_p
@@ -154,8 +154,11 @@ def key_tile(d: int) -> int:
     return r
 
 
-def query_tile() -> int:
-    return _load().fabft_query_tile()
+def query_tile(d: int = 128) -> int:
+    """Query rows per workgroup for head dimension d (the V/VS fault tile unit)."""
+    r = _load().fabft_query_tile(int(d))
+    _check(r if r < 0 else 0, "fabft_query_tile")
+    return r
 
 
 def _shape(q, k, v):
@@ -219,7 +222,7 @@ def splitkv_default_splits(B: int, H: int, Lq: int, Lk: int, d: int) -> int:
     """A split count that gives the launch about 512 workgroups (two per CU),
     with at least 8 key tiles per split and at most 64 splits (measured on
     decode shapes: one to 64 queries over 8K-128K keys)."""
-    n_qt = -(-Lq // query_tile())
+    n_qt = -(-Lq // query_tile(d))
     tiles = -(-Lk // key_tile(d))
     return max(1, min(64, -(-512 // (B * H * n_qt)), tiles // 8))
 

@@ -204,7 +204,7 @@ def run_campaign(w, runs, out_path, seed=0, start=0, log_every=1000, sites=SITES
                 except (ValueError, KeyError):
                     pass
     q, k, v = device_inputs(w, seed)
-    bc, qt = key_tile(w.d), query_tile()
+    bc, qt = key_tile(w.d), query_tile(w.d)
     gold = {}
     t0 = time.time()
     n_new = 0

@@ -32,20 +32,21 @@ constexpr int kMaxSplits = 64;   // the merge reads one split per lane
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+bool head_dim_ok(int d) { return d == 64 || d == 96 || d == 128 || d == 256; }
+
 int validate(const void* q, const void* k, const void* v, void* o, int B, int H, int Lq,
              int Lk, int d, float scale, int* n_qt, int* grid) {
   if (!q || !k || !v || !o) return FABFT_E_NULL;
-  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
+  if (!head_dim_ok(d)) return FABFT_E_HEADDIM;
   if (B < 1 || H < 1 || Lq < 1 || Lk < 1) return FABFT_E_SHAPE;
   // K and V of one head are addressed with 32-bit byte offsets; reads past
   // the end (the last tile, padding columns at d = 96) sit up to one more
   // head size further, which must not wrap either
   if ((static_cast<long long>(Lk) + 64) * d * 4 > 0xffffffffLL) return FABFT_E_SHAPE;
-  // one operand record per (head, key tile), indexed in 32 bits
-  if (static_cast<long long>(B) * H * fabft::vrec_tiles(Lk) > INT_MAX) return FABFT_E_SHAPE;
   if (!std::isfinite(scale) || scale < 0.f) return FABFT_E_SCALE;
   if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o)) return FABFT_E_ALIGN;
-  const long long nqt = (static_cast<long long>(Lq) + fabft::kQueryTile - 1) / fabft::kQueryTile;
+  const int qtile = fabft::query_tile_for(d);
+  const long long nqt = (static_cast<long long>(Lq) + qtile - 1) / qtile;
   const long long g = static_cast<long long>(B) * H * nqt;
   // grid index and per-row index arithmetic in the kernel is 32-bit
   if (g > INT_MAX || static_cast<long long>(B) * H > INT_MAX / 2) return FABFT_E_SHAPE;
@@ -73,8 +74,6 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.nsplit = 1;
   p.split_tiles = 0;
   p.ws = nullptr;
-  p.vrec = nullptr;
-  p.ntk = 0;
   p.Lq = Lq;
   p.Lk = Lk;
   p.n_qt = n_qt;
@@ -87,48 +86,8 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   return p;
 }
 
-// Operand records of the checked forward (sumrow(V) of every key, written by
-// a pre-pass): one buffer per device, allocated on first use, replaced by a
-// larger one when a call needs more, kept until the process ends.
-constexpr int kMaxDevices = 64;
-void* g_rec[kMaxDevices] = {};
-size_t g_rec_bytes[kMaxDevices] = {};
-
-uint16_t* rec_buffer(size_t bytes) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
-  if (g_rec_bytes[dev] < bytes) {
-    if (g_rec[dev]) {
-      // launches on any stream may still read the old buffer
-      if (hipDeviceSynchronize() != hipSuccess) return nullptr;
-      (void)hipFree(g_rec[dev]);
-      g_rec[dev] = nullptr;
-      g_rec_bytes[dev] = 0;
-    }
-    void* ptr = nullptr;
-    if (hipMalloc(&ptr, bytes) != hipSuccess) return nullptr;
-    g_rec[dev] = ptr;
-    g_rec_bytes[dev] = bytes;
-  }
-  return static_cast<uint16_t*>(g_rec[dev]);
-}
-
-// sumrow(V) records of the BH heads of p, on the library stream
-int prepare_records(fabft::FwdParams& p, int BH, int d) {
-  uint16_t* rec = rec_buffer(static_cast<size_t>(fabft::vrec_bytes(BH, p.Lk)));
-  if (!rec) return FABFT_E_ALLOC;
-  if (fabft::launch_vrec(p.v, BH, p.Lk, d, rec, g_stream) != 0) return FABFT_E_LAUNCH;
-  p.vrec = rec;
-  p.ntk = static_cast<int>(fabft::vrec_tiles(p.Lk));
-  return FABFT_OK;
-}
-
 // mode 0: no checksum; 1: checksum; 2: checksum + injection/debug
-int launch(fabft::FwdParams p, int d, int causal, int mode, int BH) {
-  if (mode != 0) {
-    const int rc = prepare_records(p, BH, d);
-    if (rc != FABFT_OK) return rc;
-  }
+int launch(const fabft::FwdParams& p, int d, int causal, int mode) {
   const int rc = fabft::launch_fwd(p, d, causal != 0, mode, g_stream);
   return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
 }
@@ -144,8 +103,7 @@ int fabft_attn_fwd(const void* q, const void* k, const void* v, void* o, float* 
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   if (!resid || !flags) return FABFT_E_NULL;
-  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid), d, causal, 1,
-                B * H);
+  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid), d, causal, 1);
 }
 
 int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o, int B, int H,
@@ -154,7 +112,7 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   return launch(make_params(q, k, v, o, nullptr, nullptr, Lq, Lk, d, scale, n_qt, grid), d,
-                causal, 0, B * H);
+                causal, 0);
 }
 
 }  // extern "C"
@@ -228,7 +186,7 @@ int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o
     if (rc != FABFT_OK) return rc;
     p.f[p.nf++] = fabft::FaultDesc{f->site, f->b * H + f->h, f->row, f->col, f->tile, f->bit};
   }
-  return launch(p, d, causal, 2, B * H);
+  return launch(p, d, causal, 2);
 }
 
 int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,
@@ -254,7 +212,7 @@ void fabft_get_threshold(float* tau_rel, float* tau_abs) {
 }
 
 long long fabft_splitkv_workspace_bytes(int B, int H, int Lq, int d, int nsplit) {
-  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
+  if (!head_dim_ok(d)) return FABFT_E_HEADDIM;
   if (B < 1 || H < 1 || Lq < 1 || nsplit < 1 || nsplit > kMaxSplits) return FABFT_E_SHAPE;
   // partial outputs are kept at the kernels' compute width
   return static_cast<long long>(B) * H * Lq * nsplit *
@@ -283,8 +241,6 @@ int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v, void* o,
   p.split_tiles = (tiles + nsplit - 1) / nsplit;
   p.ws = static_cast<float*>(workspace);
   p.grid = static_cast<int>(g);
-  rc = prepare_records(p, B * H, d);
-  if (rc != FABFT_OK) return rc;
   rc = fabft::launch_fwd(p, d, causal != 0, 3, g_stream);
   if (rc != 0) return FABFT_E_LAUNCH;
   rc = fabft::launch_merge(p, d, B * H, g_stream);
@@ -324,7 +280,7 @@ int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o
       int n_qt1 = 0, grid1 = 0;
       rc = validate(qh, kh, vh, oh, 1, 1, Lq, Lk, d, scale, &n_qt1, &grid1);
       if (rc != FABFT_OK) return rc;
-      rc = launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, d, scale, n_qt1, grid1), d, causal, 1, 1);
+      rc = launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, d, scale, n_qt1, grid1), d, causal, 1);
       if (rc != FABFT_OK) return rc;
       if (fabft::launch_head_flags(fh, 1, Lq, head_flags + bh, g_stream) != 0) return FABFT_E_LAUNCH;
       if (hipMemcpyAsync(head_flags_host + bh, head_flags + bh, 1, hipMemcpyDeviceToHost,
@@ -342,7 +298,7 @@ int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o
 int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq, int d,
                        double* gsum, uint8_t* gflags) {
   if (!o || !resid || !gsum || !gflags) return FABFT_E_NULL;
-  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
+  if (!head_dim_ok(d)) return FABFT_E_HEADDIM;
   if (B < 1 || H < 1 || Lq < 1) return FABFT_E_SHAPE;
   if (static_cast<long long>(B) * H > INT_MAX) return FABFT_E_SHAPE;
   if (!aligned16(o)) return FABFT_E_ALIGN;
@@ -356,25 +312,27 @@ void fabft_set_weighted_check(int on) { g_wcheck = on ? 1 : 0; }
 int fabft_get_weighted_check(void) { return g_wcheck; }
 
 int fabft_key_tile(int d) {
-  if (d != 64 && d != 96 && d != 128) return FABFT_E_HEADDIM;
+  if (!head_dim_ok(d)) return FABFT_E_HEADDIM;
   return fabft::key_tile(d);
 }
 
-int fabft_query_tile(void) { return fabft::kQueryTile; }
+int fabft_query_tile(int d) {
+  if (!head_dim_ok(d)) return FABFT_E_HEADDIM;
+  return fabft::query_tile_for(d);
+}
 
 const char* fabft_status_str(int status) {
   switch (status) {
     case FABFT_OK: return "ok";
     case FABFT_E_NULL: return "null pointer argument";
     case FABFT_E_SHAPE: return "invalid shape (B, H, Lq, Lk must be >= 1; grid too large)";
-    case FABFT_E_HEADDIM: return "unsupported head dimension (d must be 64, 96 or 128)";
+    case FABFT_E_HEADDIM: return "unsupported head dimension (d must be 64, 96, 128 or 256)";
     case FABFT_E_ALIGN: return "q, k, v and o must be 16-byte aligned";
     case FABFT_E_LAUNCH: return "kernel launch failed";
     case FABFT_E_SCALE: return "scale must be finite and >= 0";
     case FABFT_E_FAULT: return "fault descriptor out of range";
     case FABFT_E_THRESHOLD: return "threshold must be >= 0";
     case FABFT_E_WORKSPACE: return "workspace too small (see fabft_splitkv_workspace_bytes)";
-    case FABFT_E_ALLOC: return "device memory allocation failed (sumrow buffer)";
     default: return "unknown status";
   }
 }

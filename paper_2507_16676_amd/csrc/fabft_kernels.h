@@ -7,16 +7,9 @@
 
 namespace fabft {
 
-constexpr int kQueryTile = 256;  // query rows per workgroup
-constexpr int kKeyTile = 64;     // keys per tile
-// Per key tile of a head: the small A operand of the c / l product, 8 rows
-// of kKeyTile bf16 (sumrow(V) hi, lo, ones, zeros, weighted sum hi, lo,
-// zeros, zeros), written by launch_vrec before a checked forward.
-constexpr int kRecElems = 8 * kKeyTile;
-inline long long vrec_tiles(int Lk) { return (Lk + kKeyTile - 1) / kKeyTile; }
-inline long long vrec_bytes(long long BH, int Lk) {
-  return BH * vrec_tiles(Lk) * kRecElems * 2;
-}
+// Query rows per workgroup for head dimension d: 8 waves of 32 rows, or 4
+// waves at d = 256 (one wave per SIMD, for the register file of 512).
+constexpr int query_tile_for(int d) { return d == 256 ? 128 : 256; }
 
 // One injected single-bit fault (site numbers and fields as fabft_fault,
 // with the head flattened to bh = b * H + h).
@@ -45,8 +38,6 @@ struct FwdParams {
   float* ws;
   int dio;               // head dimension of q, k, v, o in memory (<= the
                          // kernel's width; the rest of the width is zero)
-  const uint16_t* vrec;  // operand records of every head (checked modes)
-  int ntk;               // key tiles per head in vrec
   int Lq, Lk;
   int n_qt;       // query tiles per head
   int grid;       // workgroups = B * H * n_qt
@@ -60,10 +51,8 @@ struct FwdParams {
 // 3: checksum on, one key split per workgroup (partial states to p.ws)
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream);
 int key_tile(int d);
-// sumrow(V) records of BH heads (Eq. 4) into rec (vrec_bytes(BH, Lk) bytes).
-int launch_vrec(const uint16_t* v, int BH, int Lk, int d, uint16_t* rec, hipStream_t stream);
-// Width the kernels compute with for a head dimension d (64, 96 or 128): d
-// itself, or 128 for d = 96 (columns 96..127 are zero on chip).
+// Width the kernels compute with for a head dimension d (64, 96, 128 or
+// 256): d itself, or 128 for d = 96 (columns 96..127 are zero on chip).
 inline int compute_width(int d) { return d == 96 ? 128 : d; }
 // Partial-state record of (head, row, split) in the split workspace, in
 // floats: m (exp2 domain), l, c, c_w, then the d unnormalised outputs o.

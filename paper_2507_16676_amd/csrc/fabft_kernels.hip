@@ -30,17 +30,17 @@
 //  * The K rows feeding MFMA row r are permuted (bits 2 and 3 of r swapped)
 //    so that the S^T accumulator of a lane already holds, for each 16-key
 //    step of P V, the 8 consecutive keys its B operand needs.
-//  * sumrow(V) of every key is computed once per head by vrec_kernel (8
-//    threads per key, fp32 via v_dot2 and a DPP reduction) and stored as a
-//    bf16 pair hi + lo (hi = bf16(vs), lo = bf16(vs - hi);
-//    |vs - hi - lo| <= 2^-17|vs|): one sum per key shared by all query rows,
-//    the paper's shared adder. It reaches the forward kernel as an 8-row
-//    operand record per key tile [sumrow hi; sumrow lo; ones; 0; weighted
-//    hi; weighted lo; 0; 0], loaded into LDS with the K and V tiles.
+//  * sumrow(V) of a key tile is computed from LDS by the whole workgroup
+//    (8 threads per key, 4 at d = 256; fp32 via v_dot2 and a DPP reduction)
+//    while the tile before it is processed, and stored as a bf16 pair
+//    hi + lo (hi = bf16(vs), lo = bf16(vs - hi); |vs - hi - lo| <=
+//    2^-17|vs|) in an 8-row operand [sumrow hi; sumrow lo; ones; 0; weighted
+//    hi; weighted lo; 0; 0]: one sum per key and tile shared by all query rows
+//    of the workgroup, the paper's shared adder.
 //  * The weights p~ = bf16(p) feed the P V MFMA; l and the checksum c use
 //    exactly those p~, so that the rounding of P cancels between pred and
 //    actual. They come from one more 32x32x16 MFMA per 16-key step with the
-//    same P^T operand and that record as A operand: rows 0-2 of the
+//    same P^T operand and that operand as A: rows 0-2 of the
 //    accumulator are c_hi, c_lo and l of each query, rescaled like o (Eq. 10
 //    carries c as an extra row of V^T).
 //  * Lazy rescaling: the running max used for the exponentials is moved only
@@ -68,11 +68,19 @@ typedef short s16x4 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 
-constexpr int kWaves = 8;
-constexpr int kThreads = 64 * kWaves;
-constexpr int kBr = 32 * kWaves;
-static_assert(kBr == kQueryTile, "query rows per workgroup");
-constexpr int kStages = 4;               // LDS ring depth (tiles in flight + 1)
+// Workgroup shape per row width D: WAVES waves of 32 query rows, an LDS ring
+// of STAGES key tiles, AHEAD of them loading while one is in use. D = 256
+// runs one wave per SIMD (512 registers for its 256-wide Q and o fragments)
+// and a 2-stage ring (64 KiB per stage).
+template <int D>
+struct Cfg {
+  static constexpr int WAVES = D == 256 ? 4 : 8;
+  static constexpr int THREADS = 64 * WAVES;
+  static constexpr int BR = 32 * WAVES;
+  static constexpr int STAGES = D == 256 ? 2 : 4;
+  static constexpr int AHEAD = STAGES - 1;
+  static_assert(BR == query_tile_for(D), "query rows per workgroup");
+};
 constexpr int kBc = 64;                  // keys per tile
 constexpr float kLazy = 8.0f;            // max drift (exp2 domain) before a rescale
 constexpr uint32_t kOnes = 0x3f803f80u;  // bf16 pair (1.0, 1.0)
@@ -96,12 +104,14 @@ __device__ __forceinline__ float dpp(float x) {
       __builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
 }
 
-// Sum over aligned groups of 8 consecutive lanes; every lane of the group
-// receives the same value.
-__device__ __forceinline__ float group8_sum(float x) {
+// Sum over aligned groups of N (4 or 8) consecutive lanes; every lane of
+// the group receives the same value.
+template <int N>
+__device__ __forceinline__ float group_sum(float x) {
+  static_assert(N == 4 || N == 8, "group size");
   x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
   x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
-  x += dpp<0x141>(x);  // row_half_mirror
+  if constexpr (N == 8) x += dpp<0x141>(x);  // row_half_mirror
   return x;
 }
 
@@ -197,10 +207,9 @@ struct Tile {
 // and lo parts, padded to 8 rows (1 KiB per key tile: one wave-wide 16-byte
 // load). MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9 read
 // WHi, WLo (accumulator elements 4, 5 of lanes 0-31); the others read the
-// zero row. vrec_kernel writes this operand for every key tile of a head.
+// zero row.
 enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRowWLo = 5,
        kVsmRows = 8 };
-static_assert(kVsmRows * kBc == kRecElems && kBc == kKeyTile, "operand record layout");
 
 // The ring's K tiles, then its V tiles, then the small operands: with the
 // stage a compile-time constant, every operand read of a tile is a per-lane
@@ -208,9 +217,9 @@ static_assert(kVsmRows * kBc == kRecElems && kBc == kKeyTile, "operand record la
 // d = 128, the reach of the LDS offset field).
 template <int D>
 struct Ring {
-  uint16_t k[kStages][kBc * D];
-  uint16_t v[kStages][kBc * D];
-  uint16_t vsm[kStages][kVsmRows][kBc];
+  uint16_t k[Cfg<D>::STAGES][kBc * D];
+  uint16_t v[Cfg<D>::STAGES][kBc * D];
+  uint16_t vsm[Cfg<D>::STAGES][kVsmRows][kBc];
 };
 
 template <int S>
@@ -221,7 +230,12 @@ struct StageId {
 // WCHK: the weighted second checksum is compiled in (only with CHECK).
 // SPLIT: the workgroup runs one key split and writes partial row states.
 template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT>
-__global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
+__global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
+  constexpr int kWaves = Cfg<D>::WAVES;
+  constexpr int kThreads = Cfg<D>::THREADS;
+  constexpr int kBr = Cfg<D>::BR;
+  constexpr int kStages = Cfg<D>::STAGES;
+  constexpr int AHEAD = Cfg<D>::AHEAD;
   constexpr int BC = kBc;
   constexpr int CPR = Tile<D>::CPR;
   constexpr int NKB = BC / 32;    // 32-key blocks per tile
@@ -308,11 +322,10 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   float m2_run = -__builtin_inff();   // running max, exp2 domain (s * scale * log2 e)
   const float sl2 = p.sl2;
 
-  // without the checksum no record is loaded: the ones and zero rows of the
-  // c / l operand (l only) are set once in every stage (visible after the
-  // prologue barrier)
-  if constexpr (!CHECK) {
-    const int st_i = tid >> 7, row = kRowOnes + ((tid >> 6) & 1), key = tid & 63;
+  // constant rows of the c / l operand in every stage (visible after the
+  // first barrier)
+  for (int e = tid; e < kStages * 2 * BC; e += kThreads) {
+    const int st_i = e / (2 * BC), row = kRowOnes + (e / BC) % 2, key = e % BC;
     ring.vsm[st_i][row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
   }
   // row of the c / l operand that MFMA row mrow reads (rows 0, 1 only with
@@ -329,10 +342,6 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   const uint32_t kv_bytes = (uint32_t)Lk * DIO * 2;
   const i32x4 krs = buffer_rsrc(p.k + kbase, kv_bytes);
   const i32x4 vrs = buffer_rsrc(p.v + kbase, kv_bytes);
-  // the operand record of each key tile (1 KiB) is loaded by one wave
-  constexpr int kRecWave = kWaves - 1;
-  const i32x4 rrs = buffer_rsrc(CHECK ? p.vrec + (size_t)bh * p.ntk * kRecElems : p.v,
-                                CHECK ? (uint32_t)p.ntk * kRecElems * 2 : 0u);
   uint32_t kvo[NLD], vvo[NLD];
 #pragma unroll
   for (int j = 0; j < NLD; ++j) {
@@ -363,11 +372,41 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       buffer_load_lds16(krs, kvo[j], soff, wl + kOff + j * kThreads * 16);
       buffer_load_lds16(vrs, vvo[j], soff, wl + vOff + j * kThreads * 16);
     }
-    if (CHECK && wave == kRecWave) {
-      uint32_t rl = ring_lds;
-      asm volatile("" : "+s"(rl));
-      constexpr uint32_t rOff = offsetof(Ring<D>, vsm) + S * sizeof(Ring<D>::vsm[0]);
-      buffer_load_lds16(rrs, (uint32_t)lane * 16, (uint32_t)t * kRecElems * 2, rl + rOff);
+  };
+
+  // ---- sumrow(V) of the tile in stage S (Eq. 4): TPK threads per key
+  auto sumrow = [&](auto S_) __attribute__((always_inline)) {
+    constexpr int S = decltype(S_)::value;
+    constexpr int TPK = kThreads / BC;   // threads per key
+    constexpr int CPT = CPR / TPK;       // 16-byte chunks per thread
+    static_assert(TPK * BC == kThreads && CPT * TPK == CPR, "sumrow covers the tile");
+    const uint16_t* const sv = ring.v[S];
+    uint16_t(*const svsm)[kBc] = ring.vsm[S];
+    const int key = tid / TPK, part = tid % TPK;
+    float a = 0.f, aw = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const u32x4 ch = *reinterpret_cast<const u32x4*>(&sv[Tile<D>::vidx(key, CPT * part + i)]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a = dot2(ch[e], kOnes, a);
+        // a chunk starts at an even column: pair weights (1, -1)
+        if constexpr (WCHK) aw = dot2(ch[e], kAlt, aw);
+      }
+    }
+    const float vs = group_sum<TPK>(a);
+    const float vw = WCHK ? group_sum<TPK>(aw) : 0.f;
+    if (part == 0) {
+      const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
+      const uint32_t lo = pack_bf16x2(vs - __uint_as_float(hi << 16), 0.f) & 0xffffu;
+      svsm[kRowVsHi][key] = (uint16_t)hi;
+      svsm[kRowVsLo][key] = (uint16_t)lo;
+      if constexpr (WCHK) {
+        const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
+        const uint32_t wlo = pack_bf16x2(vw - __uint_as_float(whi << 16), 0.f) & 0xffffu;
+        svsm[kRowWHi][key] = (uint16_t)whi;
+        svsm[kRowWLo][key] = (uint16_t)wlo;
+      }
     }
   };
 
@@ -602,47 +641,72 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
     }
   };
 
-  // ---- pipeline: tiles t+1 and t+2 in flight while tile t is processed
+  // ---- pipeline: AHEAD tiles loading while tile t is processed
   constexpr int LPT = 2 * NLD;   // loads per thread per tile (K and V)
-  constexpr int LPTR = LPT + 1;  // the same for the wave that loads the record
-  const bool rec_wave = CHECK && wave == kRecWave;
-  // wait until at most n (0, 1 or 2) tiles of this wave's loads are in flight
-  auto wait_tiles = [&](int n) {
-    if (n >= 2) {
-      if (rec_wave) wait_vmcnt<2 * LPTR>();
-      else wait_vmcnt<2 * LPT>();
-    } else if (n == 1) {
-      if (rec_wave) wait_vmcnt<LPTR>();
-      else wait_vmcnt<LPT>();
-    } else {
-      wait_vmcnt<0>();
+  // wait until at most n (0 .. AHEAD-1) tiles of this wave's loads are in flight
+  auto wait_tiles = [&](int n) __attribute__((always_inline)) {
+    if constexpr (AHEAD >= 3) {
+      if (n >= 2) {
+        wait_vmcnt<2 * LPT>();
+        return;
+      }
     }
+    if constexpr (AHEAD >= 2) {
+      if (n == 1) {
+        wait_vmcnt<LPT>();
+        return;
+      }
+    }
+    wait_vmcnt<0>();
   };
   // tile t sits in stage (t - t_lo) % kStages; the loop below is unrolled
-  // kStages times so that each copy knows its stages at compile time
+  // kStages times so that each copy knows its stages at compile time. With
+  // three tiles ahead, sumrow of tile t+1 is taken at the end of step t
+  // (its loads are waited for at the top of step t); with one tile ahead,
+  // sumrow of tile t is taken in step t before the compute, behind a second
+  // barrier.
   if (t_end > t_lo) {
     issue(StageId<0>(), t_lo);
-    issue(StageId<1>(), t_lo + 1);
-    issue(StageId<2>(), t_lo + 2);
+    if constexpr (AHEAD >= 2) issue(StageId<1>(), t_lo + 1);
+    if constexpr (AHEAD >= 3) {
+      issue(StageId<2>(), t_lo + 2);
+      // first tile complete; the next two may be outstanding
+      wait_tiles(min(2, t_end - 1 - t_lo));
+      __syncthreads();
+      if constexpr (CHECK) sumrow(StageId<0>());
+    }
   }
   // A use of Q here, on every path into the loop, puts the compiler's own
   // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
-  // also waits for tiles 1 and 2) before the loop rather than inside it.
+  // also waits for the first tiles) before the loop rather than inside it.
 #pragma unroll
   for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
-  static_assert(kStages == 4, "the loop below is unrolled over four stages");
-  auto step = [&](auto S_, int t) {
+  static_assert(kStages == 4 || kStages == 2, "the loop below is unrolled over the stages");
+  static_assert(AHEAD == kStages - 1, "the stage of tile t-1 takes tile t+AHEAD");
+  auto step = [&](auto S_, int t) __attribute__((always_inline)) {
     constexpr int S = decltype(S_)::value;
-    // tile t complete (tiles t+1 and t+2 may still be in flight); after the
-    // barrier every wave is done with tile t-1, whose stage takes tile t+3
-    wait_tiles(min(2, t_end - 1 - t));
-    __syncthreads();
+    if constexpr (AHEAD >= 3) {
+      // tile t+1 complete (tile t+2 may still be in flight); after the
+      // barrier every wave is done with tile t-1, whose stage takes tile t+3
+      wait_tiles(min(1, t_end - 2 - t));
+      __syncthreads();
+    } else {
+      // tile t complete; after the barrier every wave is done with tile t-1,
+      // whose stage takes tile t+1, loading while tile t is processed
+      wait_tiles(0);
+      __syncthreads();
+      issue(StageId<(S + 1) % kStages>(), t + 1);
+      if constexpr (CHECK) {
+        sumrow(S_);
+        __syncthreads();
+      }
+    }
     if constexpr (INJECT) {
       // V site: flip a bit of V[row][col] in this workgroup's copy of the
-      // tile, after its sumrow was taken (by vrec_kernel) and before any
-      // wave reads it; the condition is uniform over the workgroup
-      // VS site (checker state): the same for the tile's sumrow record
-      // (col 0: hi part, col 1: lo part); faults apply one after another
+      // tile, after its sumrow was taken and before any wave reads it; VS
+      // site (checker state): the same for the tile's sumrow operand (col 0:
+      // hi part, col 1: lo part). The condition is uniform over the
+      // workgroup; faults apply one after another.
       bool hit = false;
       for (int fi = 0; fi < p.nf; ++fi) {
         const FaultDesc fd = p.f[fi];
@@ -662,18 +726,25 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
       if (hit) __syncthreads();
     }
     // waves whose rows see none of this tile's keys, or that hold no row
-    // below Lq, skip it (they still load for the others)
+    // below Lq, skip it (they still load and take sumrow for the others)
     if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(S_, t);
-    issue(StageId<(S + 3) % kStages>(), t + 3);
+    if constexpr (AHEAD >= 3) {
+      issue(StageId<(S + 3) % kStages>(), t + 3);
+      if constexpr (CHECK) {
+        if (t + 1 < t_end) sumrow(StageId<(S + 1) % kStages>());
+      }
+    }
   };
   for (int t = t_lo; t < t_end; t += kStages) {
     step(StageId<0>(), t);
     if (t + 1 >= t_end) break;
     step(StageId<1>(), t + 1);
-    if (t + 2 >= t_end) break;
-    step(StageId<2>(), t + 2);
-    if (t + 3 >= t_end) break;
-    step(StageId<3>(), t + 3);
+    if constexpr (kStages == 4) {
+      if (t + 2 >= t_end) break;
+      step(StageId<2 % kStages>(), t + 2);
+      if (t + 3 >= t_end) break;
+      step(StageId<3 % kStages>(), t + 3);
+    }
   }
 
   if constexpr (SPLIT) {
@@ -762,87 +833,13 @@ __global__ __launch_bounds__(kThreads, 1) void fwd_kernel(FwdParams p) {
   }
 }
 
-// ---- operand records (Eq. 4): sumrow(V)_k = sum_j V_kj and the weighted
-// sum_j (-1)^j V_kj of every key, split into bf16 hi + lo (|x - hi - lo| <=
-// 2^-17 |x|), once per key for all query tiles of the head (the paper's
-// adder shared by the query blocks). One workgroup per (head, kRecTiles key
-// tiles), 8 threads per key (fp32 via v_dot2 and a DPP reduction); keys past
-// Lk get 0. All of a thread's loads are issued before the first sum.
-constexpr int kRecTiles = 4;
-template <int D>
-__global__ __launch_bounds__(512) void vrec_kernel(const uint16_t* __restrict__ v, int Lk, int ntk,
-                                                   int dio, uint16_t* __restrict__ rec) {
-  constexpr int CPT = D / 64;   // 16-byte chunks per thread and tile (rows D wide)
-  const int nblk = (ntk + kRecTiles - 1) / kRecTiles;
-  const int g = blockIdx.x;
-  const int bh = g / nblk, t0 = (g - bh * nblk) * kRecTiles;
-  const int tid = threadIdx.x, key = tid >> 3, part = tid & 7;
-  u32x4 ch[kRecTiles][CPT];
-#pragma unroll
-  for (int i = 0; i < kRecTiles; ++i) {
-    const int gk = (t0 + i) * kBc + key;
-#pragma unroll
-    for (int c = 0; c < CPT; ++c) {
-      ch[i][c] = u32x4{0, 0, 0, 0};
-      if (t0 + i < ntk && gk < Lk && 8 * (CPT * part + c) < dio)
-        ch[i][c] = *reinterpret_cast<const u32x4*>(v + ((size_t)bh * Lk + gk) * dio +
-                                                   8 * (CPT * part + c));
-    }
-  }
-#pragma unroll
-  for (int i = 0; i < kRecTiles; ++i) {
-    if (t0 + i >= ntk) break;   // uniform over the workgroup
-    float a = 0.f, aw = 0.f;
-#pragma unroll
-    for (int c = 0; c < CPT; ++c)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        a = dot2(ch[i][c][e], kOnes, a);
-        // a chunk starts at an even column: pair weights (1, -1)
-        aw = dot2(ch[i][c][e], kAlt, aw);
-      }
-    const float vs = group8_sum(a), vw = group8_sum(aw);
-    uint16_t* r = rec + ((size_t)bh * ntk + t0 + i) * kRecElems;
-    if (part == 0) {
-      const uint32_t hi = pack_bf16x2(vs, 0.f) & 0xffffu;
-      const uint32_t lo = pack_bf16x2(vs - __uint_as_float(hi << 16), 0.f) & 0xffffu;
-      const uint32_t whi = pack_bf16x2(vw, 0.f) & 0xffffu;
-      const uint32_t wlo = pack_bf16x2(vw - __uint_as_float(whi << 16), 0.f) & 0xffffu;
-      r[kRowVsHi * kBc + key] = (uint16_t)hi;
-      r[kRowVsLo * kBc + key] = (uint16_t)lo;
-      r[kRowWHi * kBc + key] = (uint16_t)whi;
-      r[kRowWLo * kBc + key] = (uint16_t)wlo;
-    }
-    if (tid < 4 * kBc) {
-      // rows Ones, Zero and the two padding rows
-      const int which = tid / kBc;
-      const int rrow = which == 0 ? kRowOnes : which == 1 ? kRowZero : kRowWLo + which - 1;
-      r[rrow * kBc + (tid % kBc)] = which == 0 ? (uint16_t)0x3f80 : (uint16_t)0;
-    }
-  }
-}
-
-int launch_vrec(const uint16_t* v, int BH, int Lk, int d, uint16_t* rec, hipStream_t stream) {
-  const long long ntk = vrec_tiles(Lk);
-  const long long g = (long long)BH * ((ntk + kRecTiles - 1) / kRecTiles);
-  if (g < 1 || g > INT_MAX) return -1;
-  (void)hipGetLastError();
-  if (compute_width(d) == 128)
-    hipLaunchKernelGGL(vrec_kernel<128>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, d,
-                       rec);
-  else
-    hipLaunchKernelGGL(vrec_kernel<64>, dim3((unsigned)g), dim3(512), 0, stream, v, Lk, (int)ntk, d,
-                       rec);
-  return hipGetLastError() == hipSuccess ? 0 : -1;
-}
-
 template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT>
 static int launch_t(const FwdParams& p, hipStream_t stream) {
   // the thread's last-error slot may hold an error of an unrelated earlier
   // HIP call (made by the caller); clear it so that only this launch counts
   (void)hipGetLastError();
   hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK, SPLIT>), dim3(p.grid),
-                     dim3(kThreads), 0, stream, p);
+                     dim3(Cfg<D>::THREADS), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
@@ -951,7 +948,10 @@ int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream) {
   if (g > INT_MAX) return -1;
   (void)hipGetLastError();
   const dim3 grid((unsigned)g), block(64 * kMergeWaves);
-  if (compute_width(d) == 128) {
+  if (compute_width(d) == 256) {
+    if (p.wcheck) hipLaunchKernelGGL((merge_kernel<256, true>), grid, block, 0, stream, p, p.Lq);
+    else hipLaunchKernelGGL((merge_kernel<256, false>), grid, block, 0, stream, p, p.Lq);
+  } else if (compute_width(d) == 128) {
     if (p.wcheck) hipLaunchKernelGGL((merge_kernel<128, true>), grid, block, 0, stream, p, p.Lq);
     else hipLaunchKernelGGL((merge_kernel<128, false>), grid, block, 0, stream, p, p.Lq);
   } else {
@@ -962,11 +962,13 @@ int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream) {
 }
 
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream) {
-  if (compute_width(d) == 128) return launch_d<128>(p, causal, mode, stream);
+  const int dc = compute_width(d);
+  if (dc == 256) return launch_d<256>(p, causal, mode, stream);
+  if (dc == 128) return launch_d<128>(p, causal, mode, stream);
   return launch_d<64>(p, causal, mode, stream);
 }
 
-int key_tile(int d) { return (d == 64 || d == 96 || d == 128) ? kBc : 0; }
+int key_tile(int d) { return (d == 64 || d == 96 || d == 128 || d == 256) ? kBc : 0; }
 
 // ---- global check of one head (Alg. 3, the check accumulated over all
 // queries; Eq. 5 in its per-query form, Eq. 6-7): R = sum_i (pred_i -

@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9, -10):
+    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9):
         assert F.status_str(s) and F.status_str(s) != "unknown status"
     assert F.status_str(12345) == "unknown status"
 
@@ -40,7 +40,9 @@ def test_status_strings():
 def test_key_and_query_tiles():
     assert F.key_tile(128) == 64
     assert F.key_tile(64) == 64
-    assert F.query_tile() == 256
+    assert F.query_tile(128) == 256 and F.query_tile(96) == 256 and F.query_tile(64) == 256
+    assert F.query_tile(256) == 128
+    assert F.lib().fabft_query_tile(80) == F.E_HEADDIM
     assert F.key_tile(96) == 64
     with pytest.raises(F.FabftError):
         F.key_tile(80)
@@ -65,7 +67,7 @@ def test_threshold_validation_and_roundtrip():
     ((P, P, P, P, 0, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
     ((P, P, P, P, P, 0, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
     ((P, P, P, P, P, P, 1, 1, 8, 8, 80, 0, 1.0), F.E_HEADDIM),
-    ((P, P, P, P, P, P, 1, 1, 8, 8, 256, 0, 1.0), F.E_HEADDIM),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 512, 0, 1.0), F.E_HEADDIM),
     ((P, P, P, P, P, P, 0, 1, 8, 8, 128, 0, 1.0), F.E_SHAPE),
     ((P, P, P, P, P, P, 1, 0, 8, 8, 128, 0, 1.0), F.E_SHAPE),
     ((P, P, P, P, P, P, 1, 1, 0, 8, 128, 0, 1.0), F.E_SHAPE),

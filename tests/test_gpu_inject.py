@@ -93,7 +93,7 @@ def test_p_exponent_msb_flips_on_short_rows_are_flagged(golden):
 
 def test_v_site_flip(golden):
     # key 100, column 5, in the workgroup holding the second query tile
-    qt = F.query_tile()
+    qt = F.query_tile(W_INJ.d)
     lo, hi = qt, min(2 * qt, W_INJ.Lq)
     f = F.Fault("V", b=0, h=1, row=100, col=5, tile=1, bit=14)
     o, resid, flags, pred, actual = _inject(golden, f)
@@ -173,7 +173,7 @@ def test_vs_site_is_a_false_positive(golden):
     """A flip in the sumrow record of one workgroup changes pred of its rows
     that weight the key, not O: an alarm with a correct result."""
     (_, (o0, r0, f0, p0, a0)) = golden
-    qt = F.query_tile()
+    qt = F.query_tile(W_INJ.d)
     f = F.Fault("VS", b=0, h=1, row=100, col=0, tile=1, bit=14)
     o, resid, flags, pred, actual = _inject(golden, f)
     assert torch.equal(o.view(torch.int16), o0.view(torch.int16))
@@ -226,3 +226,28 @@ def test_d96_faults_on_the_last_columns():
     torch.cuda.synchronize()
     assert torch.all(buf[o0.numel():] == -7)
     assert torch.equal(ob.view(torch.int16), o0.view(torch.int16))
+
+
+def test_d256_sites_follow_the_128_row_query_tile():
+    """d = 256 runs 128 query rows per workgroup: a V fault in query tile 1
+    reaches only rows 128..255, an O fault only its row; both are flagged."""
+    w = W.Workload("inj256", 1, 2, 300, 300, 256, True, 1.0 / 16.0, seed=10)
+    qt = F.query_tile(256)
+    assert qt == 128
+    q, k, v = G.dev_inputs(W.make_inputs(w))
+    o0, r0, f0, p0, a0 = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale)
+    torch.cuda.synchronize()
+    assert int(f0.sum()) == 0
+    f = F.Fault("O", b=0, h=0, row=290, col=255, tile=4, bit=30)
+    o, resid, flags, pred, actual = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale,
+                                                      fault=f)
+    torch.cuda.synchronize()
+    assert _changed_rows(o, o0) == {(0, 0, 290)} and int(flags[0, 0, 290]) != 0
+    f = F.Fault("V", b=0, h=1, row=50, col=200, tile=1, bit=14)
+    o, resid, flags, pred, actual = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale,
+                                                      fault=f)
+    torch.cuda.synchronize()
+    changed = _changed_rows(o, o0)
+    assert changed and all(h == 1 and qt <= i < 2 * qt for _, h, i in changed)
+    flagged = set(map(tuple, (flags != 0).nonzero().cpu().numpy().tolist()))
+    assert flagged and flagged <= {(0, 1, i) for i in range(qt, 2 * qt)}

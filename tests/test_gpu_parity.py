@@ -69,7 +69,7 @@ def test_long_l32768_rows():
     _parity(w, rows=rows)
 
 
-@pytest.mark.parametrize("d", [64, 96, 128])
+@pytest.mark.parametrize("d", [64, 96, 128, 256])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("L", [1, 17, 129, 1000])
 def test_ragged_square(d, causal, L):
@@ -77,7 +77,7 @@ def test_ragged_square(d, causal, L):
     _parity(w)
 
 
-@pytest.mark.parametrize("d", [64, 96, 128])
+@pytest.mark.parametrize("d", [64, 96, 128, 256])
 @pytest.mark.parametrize("causal", [False, True])
 @pytest.mark.parametrize("Lq,Lk", [(100, 333), (333, 100), (300, 77), (1, 4096), (129, 64)])
 def test_rectangular(d, causal, Lq, Lk):
@@ -143,3 +143,9 @@ def test_streams_respected():
 def test_t1_dec_d96_full():
     """d = 96 at the Table I setting (one layer, L = 256, 32 heads)."""
     _parity(W.WORKLOADS["t1_dec_d96"])
+
+
+def test_t1_dec_d256_full():
+    """d = 256 at the Table I setting (one layer, L = 256, 16 heads): one
+    wave per SIMD, 128 query rows per workgroup."""
+    _parity(W.WORKLOADS["t1_dec_d256"])

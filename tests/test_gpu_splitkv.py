@@ -22,6 +22,7 @@ CASES = [
     (W.Workload("sq300", 1, 2, 300, 300, 128, True, 128 ** -0.5, seed=14), 3),
     (W.Workload("one", 1, 1, 5, 2000, 64, False, 0.125, seed=15), 1),
     (W.Workload("dec3d96", 2, 2, 3, 1500, 96, True, 96 ** -0.5, seed=16), 6),
+    (W.Workload("dec5d256", 1, 3, 5, 2100, 256, True, 256 ** -0.5, seed=17), 7),
 ]
 
 

@@ -21,6 +21,7 @@ CASES = [
     W.Workload("w_rect", 1, 2, 300, 1000, 128, False, 128 ** -0.5, seed=4),
     W.Workload("w_masked", 1, 2, 333, 100, 128, True, 128 ** -0.5, seed=5),
     W.Workload("w_d96", 1, 2, 200, 200, 96, True, 96 ** -0.5, seed=6),
+    W.Workload("w_d256", 1, 2, 300, 300, 256, True, 256 ** -0.5, seed=8),
 ]
 
 

@@ -119,6 +119,7 @@ WORKLOADS = {
     "t1_dec_d96": Workload("t1_dec_d96", 1, 32, 256, 256, 96, True, 1.0 / math.sqrt(96.0)),
     "t1_dec_d128": Workload("t1_dec_d128", 1, 32, 256, 256, 128, True,
                             1.0 / math.sqrt(128.0)),
+    "t1_dec_d256": Workload("t1_dec_d256", 1, 16, 256, 256, 256, True, 1.0 / 16.0),
 }
 
 
