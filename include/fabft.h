@@ -65,9 +65,11 @@ enum {
                                M = sum_j |O_ij| + |pred| */
   FABFT_FLAG_NONFINITE = 2, /* a residual, or the row's sum_j |O_ij| (so the
                                threshold), is NaN or infinite */
-  FABFT_FLAG_WEIGHTED = 4   /* weighted check only (fabft_set_weighted_check):
+  FABFT_FLAG_WEIGHTED = 4,  /* weighted check only (fabft_set_weighted_check):
                                |pred_w - actual_w| > tau_rel * M_w + tau_abs,
                                M_w = sum_j |O_ij| + |pred_w| */
+  FABFT_FLAG_SCORES = 8     /* score check only (fabft_set_score_check): see
+                               there */
 };
 
 /*
@@ -128,6 +130,32 @@ void fabft_set_stream(void* hip_stream);
  */
 int fabft_set_threshold(float tau_rel, float tau_abs);
 void fabft_get_threshold(float* tau_rel, float* tau_abs);
+
+/*
+ * Score check (an extension; off by default). The output checksum cannot see
+ * a fault in a score s_ik = q_i . k_k: p~, o, l and c all use the faulty
+ * score consistently. With a workspace set here, every checked forward
+ * (fabft_attn_fwd, the injection entry points, fabft_recompute_flagged; not
+ * the key split) also compares, per query row i, the sum of its raw scores
+ * over the key tiles that need no mask (all but the last one or two of a
+ * causal row, and the last one when Lk % 64 != 0) with q_i . sum_k K_k over
+ * the same keys (the row checksum of the product S = Q K^T), and sets
+ * FABFT_FLAG_SCORES when |lhs - rhs| > tau_s * (|q_i| . sum_k |K_k|) + tau_abs.
+ * The sums of K (and |K|) per key tile come from a pre-pass over K into the
+ * workspace on the library stream: fabft_score_check_workspace_bytes(B, H,
+ * Lk, d) bytes for a call, 16-byte aligned, caller-owned, kept in use (not
+ * copied) while set; a call whose need exceeds it returns FABFT_E_WORKSPACE.
+ * It also catches a fault in q_i that lands after the first key tile (the
+ * right-hand side uses the final q_i for all full tiles); a score fault in
+ * a masked tile, or a q fault present from the start, is not covered.
+ * d = 256 is not supported (FABFT_E_HEADDIM while the check is on).
+ * workspace = NULL switches the check off. tau_s = 0 selects the default
+ * (2^-22); a negative or NaN tau_s is FABFT_E_THRESHOLD. Process-global,
+ * not thread-safe.
+ */
+long long fabft_score_check_workspace_bytes(int B, int H, int Lk, int d);
+int fabft_set_score_check(void* workspace, long long workspace_bytes, float tau_s);
+float fabft_get_score_threshold(void);
 
 /*
  * Recompute on flag (after detection): for every head (b, h) with a flagged

@@ -28,7 +28,7 @@ _fp = ctypes.POINTER(ctypes.c_float)
 FABFT_OK = 0
 E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE = \
     -1, -2, -3, -4, -5, -6, -7, -8, -9
-FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED = 1, 2, 4
+FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED, FLAG_SCORES = 1, 2, 4, 8
 SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M, SITE_Q, SITE_VS = range(10)
 SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V,
          "C": SITE_C, "L": SITE_L, "M": SITE_M, "Q": SITE_Q, "VS": SITE_VS}
@@ -69,6 +69,12 @@ def _load() -> ctypes.CDLL:
                                           _f, ctypes.POINTER(FabftFault), _i, _vp, _vp, _vp,
                                           _vp]
     L.fabft_attn_fwd_inject_n.restype = _i
+    L.fabft_score_check_workspace_bytes.argtypes = [_i, _i, _i, _i]
+    L.fabft_score_check_workspace_bytes.restype = ctypes.c_longlong
+    L.fabft_set_score_check.argtypes = [_vp, ctypes.c_longlong, _f]
+    L.fabft_set_score_check.restype = _i
+    L.fabft_get_score_threshold.argtypes = []
+    L.fabft_get_score_threshold.restype = _f
     L.fabft_set_stream.argtypes = [_vp]
     L.fabft_set_stream.restype = None
     L.fabft_set_threshold.argtypes = [_f, _f]
@@ -101,7 +107,8 @@ def _load() -> ctypes.CDLL:
 
 
 EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
-           "fabft_attn_fwd_inject_n",
+           "fabft_attn_fwd_inject_n", "fabft_score_check_workspace_bytes",
+           "fabft_set_score_check", "fabft_get_score_threshold",
            "fabft_attn_fwd_splitkv", "fabft_splitkv_workspace_bytes",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
            "fabft_global_check", "fabft_recompute_flagged",
@@ -137,6 +144,33 @@ def get_threshold() -> tuple[float, float]:
     a, b = ctypes.c_float(), ctypes.c_float()
     _load().fabft_get_threshold(ctypes.byref(a), ctypes.byref(b))
     return a.value, b.value
+
+
+def score_check_workspace_bytes(B: int, H: int, Lk: int, d: int) -> int:
+    r = _load().fabft_score_check_workspace_bytes(B, H, Lk, d)
+    _check(int(r) if r < 0 else 0, "fabft_score_check_workspace_bytes")
+    return int(r)
+
+
+_SCORE_WS = None   # keeps the workspace tensor alive while the check is on
+
+
+def set_score_check(workspace=None, tau_s: float = 0.0):
+    """Switch the score check on with a device workspace (a tensor of at
+    least score_check_workspace_bytes bytes), or off with None."""
+    global _SCORE_WS
+    if workspace is None:
+        _check(_load().fabft_set_score_check(None, 0, 0.0), "fabft_set_score_check")
+        _SCORE_WS = None
+        return
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(_load().fabft_set_score_check(workspace.data_ptr(), nbytes, float(tau_s)),
+           "fabft_set_score_check")
+    _SCORE_WS = workspace
+
+
+def get_score_threshold() -> float:
+    return float(_load().fabft_get_score_threshold())
 
 
 def set_weighted_check(on: bool):
@@ -351,6 +385,7 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
 __all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_splitkv", "splitkv_workspace_bytes",
            "splitkv_default_splits",
            "global_check", "recompute_flagged", "Fault", "FabftError", "set_threshold",
+           "set_score_check", "score_check_workspace_bytes", "get_score_threshold",
            "get_threshold", "set_weighted_check", "get_weighted_check", "key_tile",
            "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "MAX_FAULTS", "FLAG_RESID",
-           "FLAG_NONFINITE", "FLAG_WEIGHTED"]
+           "FLAG_NONFINITE", "FLAG_WEIGHTED", "FLAG_SCORES"]

@@ -26,6 +26,14 @@ float g_tau_abs = 0.0f;
 // Weighted second checksum (weights (-1)^j) next to the paper's one; off by
 // default, so that the default path is the paper's single check.
 int g_wcheck = 0;
+// Score check (off: null): caller-provided workspace for the K column sums,
+// and its relative threshold. The largest fault-free |lhs - rhs| /
+// (|q| . sum|K|) seen on the benchmark workloads lies between 2^-26 and
+// 2^-25; 2^-22 leaves an 8x margin.
+void* g_sws = nullptr;
+long long g_sws_bytes = 0;
+constexpr float kTauScoreDefault = 1.0f / 4194304.0f;
+float g_tau_s = kTauScoreDefault;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxSplits = 64;   // the merge reads one split per lane
@@ -83,11 +91,30 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.tau_abs = g_tau_abs;
   p.nf = 0;
   for (int i = 0; i < fabft::kMaxFaults; ++i) p.f[i] = fabft::FaultDesc{0, -1, -1, -1, -1, -1};
+  p.kpre = p.kabs = nullptr;
+  p.ntk = 0;
+  p.tau_s = g_tau_s;
   return p;
 }
 
-// mode 0: no checksum; 1: checksum; 2: checksum + injection/debug
-int launch(const fabft::FwdParams& p, int d, int causal, int mode) {
+long long score_ws_bytes(long long BH, int Lk, int d) {
+  return 2 * fabft::kpre_floats(BH, Lk, d) * static_cast<long long>(sizeof(float));
+}
+
+// mode 0: no checksum; 1: checksum; 2: checksum + injection/debug. With the
+// score check switched on, modes 1 and 2 first write the K column sums of
+// the BH heads into its workspace.
+int launch(fabft::FwdParams p, int d, int causal, int mode, int BH) {
+  if (g_sws && (mode == 1 || mode == 2)) {
+    if (d == 256) return FABFT_E_HEADDIM;
+    if (score_ws_bytes(BH, p.Lk, d) > g_sws_bytes) return FABFT_E_WORKSPACE;
+    float* kpre = static_cast<float*>(g_sws);
+    float* kabs = kpre + fabft::kpre_floats(BH, p.Lk, d);
+    if (fabft::launch_kpre(p.k, BH, p.Lk, d, kpre, kabs, g_stream) != 0) return FABFT_E_LAUNCH;
+    p.kpre = kpre;
+    p.kabs = kabs;
+    p.ntk = (p.Lk + 63) / 64;
+  }
   const int rc = fabft::launch_fwd(p, d, causal != 0, mode, g_stream);
   return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
 }
@@ -103,7 +130,8 @@ int fabft_attn_fwd(const void* q, const void* k, const void* v, void* o, float* 
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   if (!resid || !flags) return FABFT_E_NULL;
-  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid), d, causal, 1);
+  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid), d, causal, 1,
+                B * H);
 }
 
 int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o, int B, int H,
@@ -112,7 +140,7 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
   return launch(make_params(q, k, v, o, nullptr, nullptr, Lq, Lk, d, scale, n_qt, grid), d,
-                causal, 0);
+                causal, 0, B * H);
 }
 
 }  // extern "C"
@@ -186,7 +214,7 @@ int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o
     if (rc != FABFT_OK) return rc;
     p.f[p.nf++] = fabft::FaultDesc{f->site, f->b * H + f->h, f->row, f->col, f->tile, f->bit};
   }
-  return launch(p, d, causal, 2);
+  return launch(p, d, causal, 2, B * H);
 }
 
 int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,
@@ -280,7 +308,7 @@ int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o
       int n_qt1 = 0, grid1 = 0;
       rc = validate(qh, kh, vh, oh, 1, 1, Lq, Lk, d, scale, &n_qt1, &grid1);
       if (rc != FABFT_OK) return rc;
-      rc = launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, d, scale, n_qt1, grid1), d, causal, 1);
+      rc = launch(make_params(qh, kh, vh, oh, rh, fh, Lq, Lk, d, scale, n_qt1, grid1), d, causal, 1, 1);
       if (rc != FABFT_OK) return rc;
       if (fabft::launch_head_flags(fh, 1, Lq, head_flags + bh, g_stream) != 0) return FABFT_E_LAUNCH;
       if (hipMemcpyAsync(head_flags_host + bh, head_flags + bh, 1, hipMemcpyDeviceToHost,
@@ -308,6 +336,30 @@ int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq, 
 }
 
 void fabft_set_weighted_check(int on) { g_wcheck = on ? 1 : 0; }
+
+long long fabft_score_check_workspace_bytes(int B, int H, int Lk, int d) {
+  if (!head_dim_ok(d) || d == 256) return FABFT_E_HEADDIM;
+  if (B < 1 || H < 1 || Lk < 1) return FABFT_E_SHAPE;
+  return score_ws_bytes(static_cast<long long>(B) * H, Lk, d);
+}
+
+int fabft_set_score_check(void* workspace, long long workspace_bytes, float tau_s) {
+  if (!workspace) {
+    g_sws = nullptr;
+    g_sws_bytes = 0;
+    g_tau_s = kTauScoreDefault;
+    return FABFT_OK;
+  }
+  if (!aligned16(workspace)) return FABFT_E_ALIGN;
+  if (workspace_bytes < 1) return FABFT_E_WORKSPACE;
+  if (!std::isfinite(tau_s) || tau_s < 0.f) return FABFT_E_THRESHOLD;
+  g_sws = workspace;
+  g_sws_bytes = workspace_bytes;
+  g_tau_s = tau_s > 0.f ? tau_s : kTauScoreDefault;
+  return FABFT_OK;
+}
+
+float fabft_get_score_threshold(void) { return g_tau_s; }
 
 int fabft_get_weighted_check(void) { return g_wcheck; }
 

@@ -38,6 +38,13 @@ struct FwdParams {
   float* ws;
   int dio;               // head dimension of q, k, v, o in memory (<= the
                          // kernel's width; the rest of the width is zero)
+  // score check (modes 1, 2; null = off): per head, ntk + 1 rows of the
+  // kernel's width D, the exclusive prefix over key tiles of the column sums
+  // of K (kpre) and of |K| (kabs); tau_s its relative threshold
+  const float* kpre;
+  const float* kabs;
+  int ntk;
+  float tau_s;
   int Lq, Lk;
   int n_qt;       // query tiles per head
   int grid;       // workgroups = B * H * n_qt
@@ -60,6 +67,14 @@ inline int split_record_floats(int d) { return d + 4; }
 // Merge the partial states of every row (mode 3 writes them) into O, resid
 // and flags.
 int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream);
+// Column sums of K per key tile and their exclusive prefix over the tiles
+// (kpre) and the same for |K| (kabs): BH heads, (ceil(Lk/64) + 1) rows of
+// compute_width(d) floats each.
+int launch_kpre(const uint16_t* k, int BH, int Lk, int d, float* kpre, float* kabs,
+                hipStream_t stream);
+inline long long kpre_floats(long long BH, int Lk, int d) {
+  return BH * ((Lk + 63) / 64 + 1) * (long long)compute_width(d);
+}
 int launch_head_flags(const uint8_t* flags, int BH, int Lq, uint8_t* hflags, hipStream_t stream);
 int launch_global(const uint16_t* o, const float* resid, int BH, int Lq, int d, float tau_rel,
                   float tau_abs, double* gsum, uint8_t* gflag, hipStream_t stream);

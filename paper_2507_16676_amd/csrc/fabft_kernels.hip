@@ -229,7 +229,8 @@ struct StageId {
 
 // WCHK: the weighted second checksum is compiled in (only with CHECK).
 // SPLIT: the workgroup runs one key split and writes partial row states.
-template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT>
+// SCHK: the score check is compiled in (only with CHECK, not with SPLIT).
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false>
 __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
   constexpr int kWaves = Cfg<D>::WAVES;
   constexpr int kThreads = Cfg<D>::THREADS;
@@ -319,6 +320,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
   for (int b = 0; b < NDB; ++b) oacc[b] = f32x16{};
   f32x16 aux = {};                    // lanes < 32: [0] c_hi, [1] c_lo, [2] l of query mrow
+  float s_lhs = 0.f;                  // score check: sum of this lane's scores in full tiles
   float m2_run = -__builtin_inff();   // running max, exp2 domain (s * scale * log2 e)
   const float sl2 = p.sl2;
 
@@ -478,6 +480,17 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
       }
     }
 
+    if constexpr (SCHK) {
+      // score check: sum of the scores of full (unmasked) tiles as they
+      // enter the softmax (Section II's row checksum of a matrix product,
+      // applied to S = Q K^T)
+      if (!need_mask) {
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) s_lhs += sacc[kb][i];
+      }
+    }
     // mask, tile max (Alg. 3: m_i = max(m_{i-1}, s_i))
     if (need_mask) {
 #pragma unroll
@@ -818,6 +831,44 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
       nonfinite = nonfinite || nonfinite_bits(rw);
       if (!(__builtin_fabsf(rw) <= p.tau_rel * (absum + __builtin_fabsf(pred_w)) + p.tau_abs)) f |= 4;
     }
+    if constexpr (SCHK) {
+      // score check: sum over the full key tiles of s_ij against
+      // q_i . sum_k K_k over the same keys (the prefix of the K column sums
+      // up to the wave's first masked tile), within tau_s * |q_i| . sum_k |K_k|
+      int tw = Lk / BC;   // tiles without the key-range mask
+      if (CAUSAL) {
+        const int lim = wq_lo + off + 1;   // tiles wholly below the wave's diagonal
+        tw = min(tw, lim <= 0 ? 0 : lim / BC);
+      }
+      const size_t kro = ((size_t)bh * (p.ntk + 1) + tw) * D;
+      float rhs = 0.f, ms = 0.f;
+#pragma unroll
+      for (int s2 = 0; s2 < NDS; ++s2) {
+        const int c0 = 16 * s2 + 8 * grp;   // the lane's 8 columns of q
+        const f32x4 kp0 = *reinterpret_cast<const f32x4*>(p.kpre + kro + c0);
+        const f32x4 kp1 = *reinterpret_cast<const f32x4*>(p.kpre + kro + c0 + 4);
+        const f32x4 ka0 = *reinterpret_cast<const f32x4*>(p.kabs + kro + c0);
+        const f32x4 ka1 = *reinterpret_cast<const f32x4*>(p.kabs + kro + c0 + 4);
+        const float kp[8] = {kp0[0], kp0[1], kp0[2], kp0[3], kp1[0], kp1[1], kp1[2], kp1[3]};
+        const float ka[8] = {ka0[0], ka0[1], ka0[2], ka0[3], ka1[0], ka1[1], ka1[2], ka1[3]};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float qa = __uint_as_float(qf[s2][e] << 16);
+          const float qb = __uint_as_float(qf[s2][e] & 0xffff0000u);
+          rhs = __builtin_fmaf(qa, kp[2 * e], __builtin_fmaf(qb, kp[2 * e + 1], rhs));
+          ms = __builtin_fmaf(__builtin_fabsf(qa), ka[2 * e],
+                              __builtin_fmaf(__builtin_fabsf(qb), ka[2 * e + 1], ms));
+        }
+      }
+      // scores carry the softmax scale only in the exponent (exp2 of s * sl2):
+      // the sums compare raw q . k
+      const float lhs = sum_xor32(s_lhs);
+      rhs = sum_xor32(rhs);
+      ms = sum_xor32(ms);
+      const float rs = lhs - rhs;
+      nonfinite = nonfinite || nonfinite_bits(rs);
+      if (!(__builtin_fabsf(rs) <= p.tau_s * ms + p.tau_abs)) f |= 8;
+    }
     if (nonfinite) f |= 3;
     if (grp == 0 && qrow < Lq) {
       const size_t ri = (size_t)bh * Lq + qrow;
@@ -833,12 +884,12 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
   }
 }
 
-template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT>
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false>
 static int launch_t(const FwdParams& p, hipStream_t stream) {
   // the thread's last-error slot may hold an error of an unrelated earlier
   // HIP call (made by the caller); clear it so that only this launch counts
   (void)hipGetLastError();
-  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK, SPLIT>), dim3(p.grid),
+  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK, SPLIT, SCHK>), dim3(p.grid),
                      dim3(Cfg<D>::THREADS), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
@@ -848,6 +899,17 @@ static int launch_c(const FwdParams& p, int mode, hipStream_t s) {
   // mode 0: no checksum, 1: checksum, 2: checksum + injection/debug,
   // 3: checksum, key split
   if (mode == 0) return launch_t<D, CAUSAL, false, false, false, false>(p, s);
+  if constexpr (D != 256) {
+    // the score check (not built for the one-wave-per-SIMD width 256)
+    if (p.kpre && (mode == 1 || mode == 2)) {
+      if (mode == 1) {
+        if (p.wcheck) return launch_t<D, CAUSAL, true, false, true, false, true>(p, s);
+        return launch_t<D, CAUSAL, true, false, false, false, true>(p, s);
+      }
+      if (p.wcheck) return launch_t<D, CAUSAL, true, true, true, false, true>(p, s);
+      return launch_t<D, CAUSAL, true, true, false, false, true>(p, s);
+    }
+  }
   if (mode == 1) {
     if (p.wcheck) return launch_t<D, CAUSAL, true, false, true, false>(p, s);
     return launch_t<D, CAUSAL, true, false, false, false>(p, s);
@@ -1016,6 +1078,71 @@ __global__ __launch_bounds__(kGThreads) void global_check_kernel(
     gsum[bh] = R;
     gflag[bh] = f;
   }
+}
+
+// ---- score check operands: column sums of K and |K| per key tile (one
+// workgroup per (head, tile), one thread per column), then per head the
+// exclusive prefix over the tiles in place (one thread per column): row t
+// holds the sums over tiles 0 .. t-1, row ntk the sums over all keys.
+// Columns past dio (d = 96) stay zero.
+template <int D>
+__global__ __launch_bounds__(D) void ksum_kernel(const uint16_t* __restrict__ k, int Lk, int ntk,
+                                                 int dio, float* __restrict__ kpre,
+                                                 float* __restrict__ kabs) {
+  const int g = blockIdx.x;
+  const int bh = g / ntk, t = g - bh * ntk;
+  const int j = threadIdx.x;
+  float a = 0.f, b = 0.f;
+  if (j < dio) {
+    const uint16_t* col = k + ((size_t)bh * Lk + (size_t)t * kBc) * dio + j;
+    const int n = min(kBc, Lk - t * kBc);
+    for (int r = 0; r < n; ++r) {
+      const float x = __uint_as_float((uint32_t)col[(size_t)r * dio] << 16);
+      a += x;
+      b += __builtin_fabsf(x);
+    }
+  }
+  const size_t o = ((size_t)bh * (ntk + 1) + t) * D + j;
+  kpre[o] = a;
+  kabs[o] = b;
+}
+
+template <int D>
+__global__ __launch_bounds__(D) void kscan_kernel(int ntk, float* __restrict__ kpre,
+                                                  float* __restrict__ kabs) {
+  const int bh = blockIdx.x, j = threadIdx.x;
+  float* pa = kpre + (size_t)bh * (ntk + 1) * D + j;
+  float* pb = kabs + (size_t)bh * (ntk + 1) * D + j;
+  float ra = 0.f, rb = 0.f;
+  for (int t = 0; t < ntk; ++t) {
+    const float a = pa[(size_t)t * D], b = pb[(size_t)t * D];
+    pa[(size_t)t * D] = ra;
+    pb[(size_t)t * D] = rb;
+    ra += a;
+    rb += b;
+  }
+  pa[(size_t)ntk * D] = ra;
+  pb[(size_t)ntk * D] = rb;
+}
+
+int launch_kpre(const uint16_t* k, int BH, int Lk, int d, float* kpre, float* kabs,
+                hipStream_t stream) {
+  const int ntk = (Lk + kBc - 1) / kBc;
+  const long long g = (long long)BH * ntk;
+  if (g < 1 || g > INT_MAX) return -1;
+  (void)hipGetLastError();
+  if (compute_width(d) == 128) {
+    hipLaunchKernelGGL(ksum_kernel<128>, dim3((unsigned)g), dim3(128), 0, stream, k, Lk, ntk, d,
+                       kpre, kabs);
+    hipLaunchKernelGGL(kscan_kernel<128>, dim3(BH), dim3(128), 0, stream, ntk, kpre, kabs);
+  } else if (compute_width(d) == 64) {
+    hipLaunchKernelGGL(ksum_kernel<64>, dim3((unsigned)g), dim3(64), 0, stream, k, Lk, ntk, d,
+                       kpre, kabs);
+    hipLaunchKernelGGL(kscan_kernel<64>, dim3(BH), dim3(64), 0, stream, ntk, kpre, kabs);
+  } else {
+    return -1;
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
 // ---- per-head OR of the row flags (one workgroup per head)

@@ -187,3 +187,26 @@ def test_recompute_flagged_validation():
     assert L.fabft_recompute_flagged(*bad_d, *ok) == F.E_HEADDIM
     no_flags = base[:5] + (None,) + base[6:]
     assert L.fabft_recompute_flagged(*no_flags, *ok) == F.E_NULL
+
+
+def test_score_check_workspace_and_switch():
+    L = F.lib()
+    ntk = (4096 + 63) // 64
+    assert F.score_check_workspace_bytes(2, 3, 4096, 128) == 2 * 2 * 3 * (ntk + 1) * 128 * 4
+    assert F.score_check_workspace_bytes(1, 1, 100, 96) == 2 * (2 + 1) * 128 * 4
+    assert L.fabft_score_check_workspace_bytes(1, 1, 100, 256) == F.E_HEADDIM
+    assert L.fabft_score_check_workspace_bytes(0, 1, 100, 64) == F.E_SHAPE
+    assert L.fabft_set_score_check(P + 8, 1024, 0.0) == F.E_ALIGN
+    assert L.fabft_set_score_check(P, 0, 0.0) == F.E_WORKSPACE
+    assert L.fabft_set_score_check(P, 1024, -1.0) == F.E_THRESHOLD
+    assert L.fabft_set_score_check(P, 1024, float("nan")) == F.E_THRESHOLD
+    try:
+        assert L.fabft_set_score_check(P, 1024, 0.0) == F.FABFT_OK
+        assert L.fabft_get_score_threshold() == pytest.approx(2.0 ** -22)
+        # a call that needs more than the workspace is rejected before a launch
+        assert L.fabft_attn_fwd(P, P, P, P, P, P, 1, 2, 8, 5000, 128, 1, 0.1) == F.E_WORKSPACE
+        assert L.fabft_attn_fwd(P, P, P, P, P, P, 1, 2, 8, 8, 256, 1, 0.1) == F.E_HEADDIM
+        assert L.fabft_set_score_check(P, 1024, 1e-3) == F.FABFT_OK
+        assert L.fabft_get_score_threshold() == pytest.approx(1e-3)
+    finally:
+        assert L.fabft_set_score_check(None, 0, 0.0) == F.FABFT_OK
