@@ -162,6 +162,8 @@ def main():
                          "forward on decode shapes (few queries, many keys), one JSON line each")
     ap.add_argument("--weighted", action="store_true",
                     help="also run the weighted second checksum (an extension)")
+    ap.add_argument("--score-check", action="store_true",
+                    help="also run the score check (an extension; its K-sum pre-pass is timed)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one plain device copy of this size (calibrates "
@@ -187,6 +189,10 @@ def main():
     torch.cuda.set_device(dev)
     log(f"[bench] workload {w.name}: B{w.B} H{w.H} Lq{w.Lq} Lk{w.Lk} d{w.d} causal={w.causal}")
     q, k, v = make_device_inputs(w, dev)
+    if args.score_check:
+        sws = torch.empty(F.score_check_workspace_bytes(w.B, w.H, w.Lk, w.d), dtype=torch.uint8,
+                          device=dev)
+        F.set_score_check(sws)
     o = torch.empty_like(q)
     resid = torch.empty((w.B, w.H, w.Lq), dtype=torch.float32, device=dev)
     flags = torch.empty((w.B, w.H, w.Lq), dtype=torch.uint8, device=dev)
@@ -273,7 +279,8 @@ def main():
         "dtype": "bf16", "data": "synthetic (seeded N(0,1), drawn on the GPU)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "Lq": w.Lq, "Lk": w.Lk,
                    "d": w.d, "causal": w.causal, "scale": w.scale,
-                   "checksum": "on+weighted" if args.weighted else "on"},
+                   "checksum": "on" + ("+weighted" if args.weighted else "")
+                               + ("+scores" if args.score_check else "")},
         "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4),
         "checksum_off": {"ms_per_step": round(ms_off, 5), "tflops": round(tflops_off, 2)},
         "checksum_overhead_pct": round(overhead, 3),

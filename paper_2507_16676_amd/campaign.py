@@ -380,6 +380,8 @@ def main(argv=None):
     c.add_argument("--summary")
     c.add_argument("--weighted", action="store_true",
                    help="also run the weighted (alternating-sign) checksum")
+    c.add_argument("--score-check", action="store_true",
+                   help="also run the score check (row sums of Q K^T)")
     c.add_argument("--sites", default=None,
                    help="comma-separated fault sites to draw from (S,P,O,V,C,L,M,Q,VS); "
                         "default S,P,O,V, or Q,O,M,L,C with --storage-weighted")
@@ -402,6 +404,13 @@ def main(argv=None):
         from . import set_weighted_check
         set_weighted_check(True)
     if a.cmd == "campaign":
+        if a.score_check:
+            import torch
+            from . import score_check_workspace_bytes, set_score_check
+            # the campaign recomputes one head per run
+            ws = torch.empty(score_check_workspace_bytes(1, 1, w.Lk, w.d), dtype=torch.uint8,
+                             device="cuda")
+            set_score_check(ws)
         sites = tuple(a.sites.split(",")) if a.sites else (
             PAPER_SITES if a.storage_weighted else SITES)
         weights = storage_weights(w, sites) if a.storage_weighted else None
@@ -414,6 +423,7 @@ def main(argv=None):
         summ["site_weights"] = None if weights is None else [float(x) for x in weights]
         summ["faults_per_run"] = [kmin, kmax]
         summ["weighted_check"] = bool(a.weighted)
+        summ["score_check"] = bool(a.score_check)
         txt = json.dumps(summ, indent=1)
         if a.summary:
             with open(a.summary, "w") as f:

@@ -1081,30 +1081,65 @@ __global__ __launch_bounds__(kGThreads) void global_check_kernel(
 }
 
 // ---- score check operands: column sums of K and |K| per key tile (one
-// workgroup per (head, tile), one thread per column), then per head the
+// workgroup of 256 threads per (head, tile): 16-byte loads of 8 columns of
+// 4 rows per thread, partial sums reduced through LDS), then per head the
 // exclusive prefix over the tiles in place (one thread per column): row t
 // holds the sums over tiles 0 .. t-1, row ntk the sums over all keys.
 // Columns past dio (d = 96) stay zero.
+constexpr int kSumThreads = 256;
 template <int D>
-__global__ __launch_bounds__(D) void ksum_kernel(const uint16_t* __restrict__ k, int Lk, int ntk,
-                                                 int dio, float* __restrict__ kpre,
-                                                 float* __restrict__ kabs) {
+__global__ __launch_bounds__(kSumThreads) void ksum_kernel(const uint16_t* __restrict__ k, int Lk,
+                                                           int ntk, int dio,
+                                                           float* __restrict__ kpre,
+                                                           float* __restrict__ kabs) {
+  constexpr int CPR = D / 8;                 // 16-byte chunks per row
+  constexpr int RG = kSumThreads / CPR;      // row groups
+  constexpr int RPG = kBc / RG;              // rows per group
+  static_assert(RG * CPR == kSumThreads && RPG * RG == kBc, "ksum layout");
+  __shared__ float part_a[RG][D];
+  __shared__ float part_b[RG][D];
   const int g = blockIdx.x;
   const int bh = g / ntk, t = g - bh * ntk;
-  const int j = threadIdx.x;
-  float a = 0.f, b = 0.f;
-  if (j < dio) {
-    const uint16_t* col = k + ((size_t)bh * Lk + (size_t)t * kBc) * dio + j;
-    const int n = min(kBc, Lk - t * kBc);
-    for (int r = 0; r < n; ++r) {
-      const float x = __uint_as_float((uint32_t)col[(size_t)r * dio] << 16);
-      a += x;
-      b += __builtin_fabsf(x);
+  const int c = threadIdx.x % CPR, rg = threadIdx.x / CPR;
+  float a[8] = {}, b[8] = {};
+  if (8 * c < dio) {
+    u32x4 ch[RPG];
+#pragma unroll
+    for (int r = 0; r < RPG; ++r) {
+      const int row = t * kBc + rg * RPG + r;
+      ch[r] = u32x4{0, 0, 0, 0};
+      if (row < Lk)
+        ch[r] = *reinterpret_cast<const u32x4*>(k + ((size_t)bh * Lk + row) * dio + 8 * c);
     }
+#pragma unroll
+    for (int r = 0; r < RPG; ++r)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x0 = __uint_as_float(ch[r][e] << 16);
+        const float x1 = __uint_as_float(ch[r][e] & 0xffff0000u);
+        a[2 * e] += x0;
+        a[2 * e + 1] += x1;
+        b[2 * e] += __builtin_fabsf(x0);
+        b[2 * e + 1] += __builtin_fabsf(x1);
+      }
   }
-  const size_t o = ((size_t)bh * (ntk + 1) + t) * D + j;
-  kpre[o] = a;
-  kabs[o] = b;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    part_a[rg][8 * c + e] = a[e];
+    part_b[rg][8 * c + e] = b[e];
+  }
+  __syncthreads();
+  for (int j = threadIdx.x; j < D; j += kSumThreads) {
+    float sa = 0.f, sb = 0.f;
+#pragma unroll
+    for (int r = 0; r < RG; ++r) {
+      sa += part_a[r][j];
+      sb += part_b[r][j];
+    }
+    const size_t o = ((size_t)bh * (ntk + 1) + t) * D + j;
+    kpre[o] = sa;
+    kabs[o] = sb;
+  }
 }
 
 template <int D>
@@ -1114,7 +1149,25 @@ __global__ __launch_bounds__(D) void kscan_kernel(int ntk, float* __restrict__ k
   float* pa = kpre + (size_t)bh * (ntk + 1) * D + j;
   float* pb = kabs + (size_t)bh * (ntk + 1) * D + j;
   float ra = 0.f, rb = 0.f;
-  for (int t = 0; t < ntk; ++t) {
+  // blocks of 8 tiles: the loads of a block are issued before its sums
+  constexpr int U = 8;
+  int t = 0;
+  for (; t + U <= ntk; t += U) {
+    float va[U], vb[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      va[u] = pa[(size_t)(t + u) * D];
+      vb[u] = pb[(size_t)(t + u) * D];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      pa[(size_t)(t + u) * D] = ra;
+      pb[(size_t)(t + u) * D] = rb;
+      ra += va[u];
+      rb += vb[u];
+    }
+  }
+  for (; t < ntk; ++t) {
     const float a = pa[(size_t)t * D], b = pb[(size_t)t * D];
     pa[(size_t)t * D] = ra;
     pb[(size_t)t * D] = rb;
@@ -1132,12 +1185,12 @@ int launch_kpre(const uint16_t* k, int BH, int Lk, int d, float* kpre, float* ka
   if (g < 1 || g > INT_MAX) return -1;
   (void)hipGetLastError();
   if (compute_width(d) == 128) {
-    hipLaunchKernelGGL(ksum_kernel<128>, dim3((unsigned)g), dim3(128), 0, stream, k, Lk, ntk, d,
-                       kpre, kabs);
+    hipLaunchKernelGGL(ksum_kernel<128>, dim3((unsigned)g), dim3(kSumThreads), 0, stream, k, Lk,
+                       ntk, d, kpre, kabs);
     hipLaunchKernelGGL(kscan_kernel<128>, dim3(BH), dim3(128), 0, stream, ntk, kpre, kabs);
   } else if (compute_width(d) == 64) {
-    hipLaunchKernelGGL(ksum_kernel<64>, dim3((unsigned)g), dim3(64), 0, stream, k, Lk, ntk, d,
-                       kpre, kabs);
+    hipLaunchKernelGGL(ksum_kernel<64>, dim3((unsigned)g), dim3(kSumThreads), 0, stream, k, Lk,
+                       ntk, d, kpre, kabs);
     hipLaunchKernelGGL(kscan_kernel<64>, dim3(BH), dim3(64), 0, stream, ntk, kpre, kabs);
   } else {
     return -1;
