@@ -250,7 +250,7 @@ def main():
                 "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
                 "kernel": (f"fabft::fwd_kernel<{w.d}, {str(w.causal).lower()}, true, false, "
-                           f"false, false>"),
+                           f"false, false, false>"),
                 "avg_launch_ms": round(avg_launch_ms, 5)}
 
     if args.copy_probe_mib > 0:

@@ -82,6 +82,10 @@ struct Cfg {
   static_assert(BR == query_tile_for(D), "query rows per workgroup");
 };
 constexpr int kBc = 64;                  // keys per tile
+#ifndef FABFT_CAUSAL_BAND
+#define FABFT_CAUSAL_BAND 4
+#endif
+constexpr int kCausalBand = FABFT_CAUSAL_BAND;  // heads per XCD in flight at once (causal)
 constexpr float kLazy = 8.0f;            // max drift (exp2 domain) before a rescale
 constexpr uint32_t kOnes = 0x3f803f80u;  // bf16 pair (1.0, 1.0)
 constexpr uint32_t kAlt = 0xbf803f80u;   // bf16 pair (1.0, -1.0): weights (-1)^j
@@ -257,8 +261,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
   // robin (XCD = id mod 8). Without a mask every tile costs the same: each
   // XCD takes a contiguous range of heads, so that a head's K and V stay in
   // one L2. With the causal mask the work per query tile grows with its
-  // index: all heads' heaviest tiles go first (longest job first); with a
-  // head count divisible by 8 a head still stays on one XCD.
+  // index: the heaviest tiles go first (longest job first), a band of heads
+  // at a time, and with a head count divisible by 8 a head stays on one XCD.
   const int G = p.grid;
   const int bid = blockIdx.x;
   int bh, qt, split = 0;
@@ -270,9 +274,24 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     qt = lg - bh * p.n_qt;
   } else if (CAUSAL) {
     const int BH = G / p.n_qt;
-    const int qr = bid / BH;
-    bh = bid - qr * BH;
-    qt = p.n_qt - 1 - qr;
+    if ((BH & 7) == 0) {
+      // XCD x owns heads x, x + 8, ...; it runs them kCausalBand heads at a
+      // time, each band longest tile first. The query tiles of a band stream
+      // the same few K/V tiles at about the same time, so one HBM read
+      // serves several of them from L2.
+      const int xcd = bid & 7, slot = bid >> 3;
+      const int band = slot / (kCausalBand * p.n_qt);
+      const int h0 = band * kCausalBand;
+      const int nb = min(kCausalBand, (BH >> 3) - h0);
+      const int w = slot - h0 * p.n_qt;
+      const int qr = w / nb;
+      bh = (h0 + w - qr * nb) * 8 + xcd;
+      qt = p.n_qt - 1 - qr;
+    } else {
+      const int qr = bid / BH;
+      bh = bid - qr * BH;
+      qt = p.n_qt - 1 - qr;
+    }
   } else {
     const int xcd = bid & 7;
     const int per = G >> 3, rem = G & 7;
