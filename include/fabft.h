@@ -22,7 +22,9 @@
  *    process-global state (setters are not thread-safe).
  *  - d must be 64, 96, 128 or 256 (d = 96 runs the d = 128 kernels with the
  *    columns 96..127 zero on chip: identical results, 4/3 of the work).
- *    B, H, Lq, Lk >= 1. scale must be finite and >= 0.
+ *    B, H, Lq, Lk >= 1. scale must be finite and >= 0; a scale below
+ *    2^-126 / log2(e) (zero included) runs as that value, which weighs every
+ *    visible key alike for scores below 2^100 in magnitude.
  *  - causal != 0 keeps key k for query i iff k <= i + (Lk - Lq)
  *    (bottom-right aligned; the plain lower triangle when Lq == Lk). A query
  *    row with no visible key gets O = 0, pred = actual = resid = 0, flag 0.

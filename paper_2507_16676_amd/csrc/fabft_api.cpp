@@ -86,7 +86,11 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.Lk = Lk;
   p.n_qt = n_qt;
   p.grid = grid;
-  p.sl2 = scale * kLog2e;
+  // A masked score is -inf and enters exp2 as -inf * sl2: sl2 must not be
+  // zero. Raised to 2^-126 (only scale 0 or a subnormal one is), it changes
+  // no exponential of a score below 2^100 in magnitude (s * sl2 < 2^-26 rounds
+  // away in exp2 near 1).
+  p.sl2 = std::max(scale * kLog2e, 0x1p-126f);
   p.tau_rel = g_tau_rel;
   p.tau_abs = g_tau_abs;
   p.nf = 0;

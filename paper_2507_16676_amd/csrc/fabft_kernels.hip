@@ -531,16 +531,19 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
           for (int i = 0; i < 16; ++i) s_lhs += sacc[kb][i];
       }
     }
-    // mask, tile max (Alg. 3: m_i = max(m_{i-1}, s_i))
+    // mask, tile max (Alg. 3: m_i = max(m_{i-1}, s_i)). A masked score is
+    // -inf, so its exponential below is exactly 0.
     if (need_mask) {
+      // last visible key of the row (past Lk, or past the diagonal), relative
+      // to this lane's first key of the tile
+      int lim = Lk - 1;
+      if (CAUSAL) lim = min(lim, qrow + off);
+      const int rel = lim - (kv0 + 8 * grp);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = kv0 + 32 * kb + 16 * (i >> 3) + 8 * grp + (i & 7);
-          const bool ok = key < Lk && (!CAUSAL || key <= qrow + off);
-          if (!ok) sacc[kb][i] = -__builtin_inff();
-        }
+        for (int i = 0; i < 16; ++i)
+          if (32 * kb + 16 * (i >> 3) + (i & 7) > rel) sacc[kb][i] = -__builtin_inff();
     }
     // one chain of three-input maxima (v_max3): one instruction per two scores
     float mx = __builtin_fmaxf(sacc[0][0], sacc[0][1]);
@@ -563,16 +566,6 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i)
         sacc[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][i], sl2, nm2));
-    if (need_mask) {
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = kv0 + 32 * kb + 16 * (i >> 3) + 8 * grp + (i & 7);
-          const bool ok = key < Lk && (!CAUSAL || key <= qrow + off);
-          if (!ok) sacc[kb][i] = 0.f;
-        }
-    }
     u32x4 pb[NKB][2];
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
