@@ -39,10 +39,13 @@
 //    of the workgroup, the paper's shared adder.
 //  * The weights p~ = bf16(p) feed the P V MFMA; l and the checksum c use
 //    exactly those p~, so that the rounding of P cancels between pred and
-//    actual. They come from one more 32x32x16 MFMA per 16-key step with the
-//    same P^T operand and that operand as A: rows 0-2 of the
-//    accumulator are c_hi, c_lo and l of each query, rescaled like o (Eq. 10
-//    carries c as an extra row of V^T).
+//    actual. They come from one more MFMA per 16-key step, a 16x16x32 whose
+//    B operand is the same P^T register and whose A operand is the 8-row
+//    sum operand: accumulator elements 0-2 of lanes 0-31 are c_hi, c_lo and
+//    l of their query, rescaled like o (Eq. 10 carries c as an extra row of
+//    V^T).
+//  * Masking (causal diagonal tiles, the ragged last tile) sets a score to
+//    -inf, whose exponential is exactly 0.
 //  * Lazy rescaling: the running max used for the exponentials is moved only
 //    when a tile's max exceeds it by more than 8 in the exp2 domain, so
 //    p <= 256 and o, l, c are rescaled (alpha != 1) rarely; o*alpha is
