@@ -66,10 +66,7 @@ enum {
   FABFT_FLAG_RESID = 1,     /* |pred - actual| > tau_rel * M + tau_abs, where
                                M = sum_j |O_ij| + |pred| */
   FABFT_FLAG_NONFINITE = 2, /* a residual, or the row's sum_j |O_ij| (so the
-                               threshold), is NaN or infinite. Row i and row
-                               i ^ 16 share one c / l product: a non-finite
-                               p~ in row i (which flags row i) makes c and l
-                               of row i ^ 16 non-finite too, and flags it */
+                               threshold), is NaN or infinite */
   FABFT_FLAG_WEIGHTED = 4,  /* weighted check only (fabft_set_weighted_check):
                                |pred_w - actual_w| > tau_rel * M_w + tau_abs,
                                M_w = sum_j |O_ij| + |pred_w| */

@@ -39,11 +39,13 @@
 //    of the workgroup, the paper's shared adder.
 //  * The weights p~ = bf16(p) feed the P V MFMA; l and the checksum c use
 //    exactly those p~, so that the rounding of P cancels between pred and
-//    actual. They come from one more MFMA per 16-key step, a 16x16x32 whose
-//    B operand is the same P^T register and whose A operand is the 8-row
-//    sum operand: accumulator elements 0-2 of lanes 0-31 are c_hi, c_lo and
-//    l of their query, rescaled like o (Eq. 10 carries c as an extra row of
-//    V^T).
+//    actual. They come from one more 32x32x16 MFMA per 16-key step with the
+//    same P^T register as B operand and the 8-row sum operand as A:
+//    accumulator elements 0-2 of lanes 0-31 are c_hi, c_lo and l of their
+//    query, rescaled like o (Eq. 10 carries c as an extra row of V^T). Each
+//    output column is one query, so a non-finite p~ in one row cannot reach
+//    the sums of another (a 16x16x32 on the same register would mix the two
+//    16-query halves of the block).
 //  * Masking (causal diagonal tiles, the ragged last tile) sets a score to
 //    -inf, whose exponential is exactly 0.
 //  * Lazy rescaling: the running max used for the exponentials is moved only
@@ -97,12 +99,6 @@ __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(
       __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
 }
-// 16x16x32: the same 8 bf16 per lane in A and B (lane l holds k-slice l / 16
-// of row / column l % 16), half the matrix-core cycles of the 32x32x16
-__device__ __forceinline__ f32x4 mfma16(u32x4 a, u32x4 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-      __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
-}
 
 // a.lo*b.lo + a.hi*b.hi + c on packed bf16 pairs, fp32 accumulate
 __device__ __forceinline__ float dot2(uint32_t a, uint32_t b, float c) {
@@ -133,11 +129,6 @@ __device__ __forceinline__ float group_sum(float x) {
 __device__ __forceinline__ float sum_xor32(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-// (x of lane l % 32, x of lane l % 32 + 32), in every lane l
-__device__ __forceinline__ f32x2 halves32(float x) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return f32x2{__uint_as_float(r[0]), __uint_as_float(r[1])};
 }
 __device__ __forceinline__ float max_xor32(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -222,15 +213,10 @@ struct Tile {
 
 // Rows of the small A operand that yields c and l: sumrow(V) as bf16 hi and
 // lo parts, ones, zeros, and the weighted row sums sum_j (-1)^j V_kj as hi
-// and lo parts, padded to 8 rows (1 KiB per key tile). The c / l product is
-// a 16x16x32 MFMA whose B operand is the 32x32x16 P~^T operand of a 16-key
-// step: its k-slice g = lane / 16 holds queries 16 (g & 1) + n and keys
-// 8 (g >> 1) .. +7 of the step. MFMA row m belongs to query half (m >> 2) & 1
-// and reads the zero row in the k-slices of the other half, so rows 0-3 give
-// [c_hi, c_lo, l, 0] of queries 0-15, rows 4-7 those of queries 16-31, and
-// rows 8-11 / 12-15 the weighted pair [w_hi, w_lo, 0, 0]: accumulator
-// elements 0-3 of lane l then belong to query l % 32, as the other
-// accumulators do.
+// and lo parts, padded to 8 rows (1 KiB per key tile: one wave-wide 16-byte
+// load). MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9 read
+// WHi, WLo (accumulator elements 4, 5 of lanes 0-31); the others read the
+// zero row.
 enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRowWLo = 5,
        kVsmRows = 8 };
 
@@ -357,7 +343,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
   f32x16 oacc[NDB];
 #pragma unroll
   for (int b = 0; b < NDB; ++b) oacc[b] = f32x16{};
-  f32x4 aux = {};   // query mrow: lanes < 32 [c_hi, c_lo, l, 0], lanes >= 32 [w_hi, w_lo, 0, 0]
+  f32x16 aux = {};                    // lanes < 32: [0] c_hi, [1] c_lo, [2] l of query mrow
   float s_lhs = 0.f;                  // score check: sum of this lane's scores in full tiles
   float m2_run = -__builtin_inff();   // running max, exp2 domain (s * scale * log2 e)
   const float sl2 = p.sl2;
@@ -368,18 +354,13 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     const int st_i = e / (2 * BC), row = kRowOnes + (e / BC) % 2, key = e % BC;
     ring.vsm[st_i][row][key] = row == kRowOnes ? (uint16_t)0x3f80 : (uint16_t)0;
   }
-  // row of the c / l operand that this lane's A slice reads (MFMA row
-  // lane % 16, k-slice lane / 16; the sum rows only with the checksum, the
-  // weighted rows only with the weighted one)
-  const int vsm_row = [&] {
-    const int m = lane & 15, ty = m & 3;
-    if (((m >> 2) & 1) != ((lane >> 4) & 1)) return (int)kRowZero;
-    if (m < 8) {
-      if (ty == 2) return (int)kRowOnes;
-      return (CHECK && ty < 2) ? (int)kRowVsHi + ty : (int)kRowZero;
-    }
-    return (WCHK && ty < 2) ? (int)kRowWHi + ty : (int)kRowZero;
-  }();
+  // row of the c / l operand that MFMA row mrow reads (rows 0, 1 only with
+  // the checksum, rows 8, 9 only with the weighted one)
+  const int vsm_row = mrow == 2                ? (int)kRowOnes
+                      : (!CHECK)               ? (int)kRowZero
+                      : mrow < 2               ? mrow
+                      : (WCHK && (mrow == 8 || mrow == 9)) ? (int)kRowWHi + (mrow - 8)
+                                               : (int)kRowZero;
 
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
   // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk read as
@@ -595,14 +576,14 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) aux[i] *= alpha;
+      for (int i = 0; i < 16; ++i) aux[i] *= alpha;
     }
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const u32x4 a = *reinterpret_cast<const u32x4*>(&svsm[vsm_row][32 * kb + 16 * h + 8 * grp]);
-        aux = mfma16(a, pb[kb][h], aux);
+        aux = mfma32(a, pb[kb][h], aux);
       }
     if constexpr (INJECT) {
       // C and L sites (checker state): a part of the fp32 accumulator pair
@@ -613,7 +594,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
             grp == 0) {
           const int el = fd.site == 5 ? fd.col : 2;   // c: hi (0) or lo (1) part
 #pragma unroll
-          for (int i = 0; i < 4; ++i)
+          for (int i = 0; i < 16; ++i)
             if (i == el) aux[i] = __uint_as_float(__float_as_uint(aux[i]) ^ (1u << fd.bit));
         }
       }
@@ -801,9 +782,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     // merge_kernel): m, l, c, c_w and the unnormalised o, in the same
     // exponent reference m (exp2 domain)
     const float l_p = sum_xor32(aux[2]);
-    const f32x2 cw = halves32(aux[0] + aux[1]);
-    const float c_p = cw[0];
-    const float cw_p = WCHK ? cw[1] : 0.f;
+    const float c_p = sum_xor32(aux[0] + aux[1]);
+    const float cw_p = WCHK ? sum_xor32(aux[4] + aux[5]) : 0.f;
     if (qrow < Lq) {
       float* rec = p.ws + (((size_t)bh * Lq + qrow) * p.nsplit + split) * (D + 4);
       if (grp == 0) *reinterpret_cast<f32x4*>(rec) = f32x4{m2_run, l_p, c_p, cw_p};
@@ -848,8 +828,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
   if constexpr (CHECK) {
     act = sum_xor32(act);
     absum = sum_xor32(absum);
-    const f32x2 cw = halves32(aux[0] + aux[1]);
-    const float pred = cw[0] * inv;
+    const float c_tot = sum_xor32(aux[0] + aux[1]);
+    const float pred = c_tot * inv;
     const float r = pred - act;
     const float M = absum + __builtin_fabsf(pred);
     // non-finite test on the bits (this file is built with relaxed NaN rules);
@@ -863,7 +843,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     float pred_w = 0.f;
     if constexpr (WCHK) {
       act_w = sum_xor32(act_w);
-      pred_w = cw[1] * inv;
+      pred_w = sum_xor32(aux[4] + aux[5]) * inv;
       const float rw = pred_w - act_w;
       nonfinite = nonfinite || nonfinite_bits(rw);
       if (!(__builtin_fabsf(rw) <= p.tau_rel * (absum + __builtin_fabsf(pred_w)) + p.tau_abs)) f |= 4;
