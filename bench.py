@@ -82,16 +82,19 @@ def time_launches(fn, steps, stream):
 DECODE_SHAPES = [(4, 32, 1, 32768), (4, 32, 16, 32768), (1, 32, 1, 131072), (8, 8, 64, 8192)]
 
 
-def decode_sweep(d: int = 128, splits=(0, 4, 8, 16, 32, 64), reps: int = 20):
+def decode_sweep(d: int = 128, splits=(0, 4, 8, 16, 32, 64), reps: int = 50, shapes=None,
+                 warm_ms: float = 100.0):
     """K/V bytes streamed per second for the one-pass forward (nsplit 0) and
-    the key-split forward on decode shapes, checksum on, non-causal."""
+    the key-split forward on decode shapes, checksum on, non-causal. Each
+    configuration first runs untimed for about `warm_ms` (the GPU clock
+    rises only under sustained load), then `reps` launches are timed."""
     import torch
     import paper_2507_16676_amd as F
     import workloads as W
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
-    for (B, H, Lq, Lk) in DECODE_SHAPES:
+    for (B, H, Lq, Lk) in (shapes or DECODE_SHAPES):
         w = W.Workload(f"decode_b{B}_h{H}_q{Lq}_k{Lk}", B, H, Lq, Lk, d, False, d ** -0.5)
         q, k, v = make_device_inputs(w, dev)
         kv_bytes = 2 * B * H * Lk * d * 2
@@ -104,7 +107,10 @@ def decode_sweep(d: int = 128, splits=(0, 4, 8, 16, 32, 64), reps: int = 20):
                                  device=dev)
                 fn = (lambda ns=ns, ws=ws: F.attn_fwd_splitkv(q, k, v, causal=False, scale=w.scale,
                                                              nsplit=ns, workspace=ws))
-            for _ in range(5):
+            fn()
+            torch.cuda.synchronize()
+            t, _ = time_launches(fn, 5, stream)
+            for _ in range(max(5, int(warm_ms / max(t / 5, 1e-3)))):
                 fn()
             t, _ = time_launches(fn, reps, stream)
             us = 1e3 * t / reps
@@ -113,6 +119,19 @@ def decode_sweep(d: int = 128, splits=(0, 4, 8, 16, 32, 64), reps: int = 20):
         print(json.dumps({"workload": w.name, "kv_bytes": kv_bytes,
                           "default_nsplit": F.splitkv_default_splits(B, H, Lq, Lk, d),
                           "results": rows}), flush=True)
+
+
+def copy_probe(mib: int, dev):
+    """One device-to-device copy of known size: the calibration launch for
+    the HBM byte counters (FETCH_SIZE, WRITE_SIZE) of a profiled run."""
+    import torch
+    n = mib * (1 << 20)
+    src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    log(f"[bench] copy probe: {mib} MiB device-to-device")
 
 
 def cpu_baseline(w, target_s: float):
@@ -157,6 +176,10 @@ def main():
     ap.add_argument("--rounds", type=int, default=5,
                     help="interleaved on/off rounds for the overhead figure")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--decode-shape", default=None,
+                    help="with --decode-sweep: one shape B,H,Lq,Lk instead of the default set")
+    ap.add_argument("--decode-splits", default=None,
+                    help="with --decode-sweep: comma-separated split counts (0 = one pass)")
     ap.add_argument("--decode-sweep", action="store_true",
                     help="instead of the benchmark line: time the one-pass and the key-split "
                          "forward on decode shapes (few queries, many keys), one JSON line each")
@@ -180,7 +203,14 @@ def main():
     import paper_2507_16676_amd as F
     F.set_weighted_check(args.weighted)
     if args.decode_sweep:
-        decode_sweep()
+        kw = {}
+        if args.decode_shape:
+            kw["shapes"] = [tuple(int(x) for x in args.decode_shape.split(","))]
+        if args.decode_splits:
+            kw["splits"] = tuple(int(x) for x in args.decode_splits.split(","))
+        decode_sweep(**kw)
+        if args.copy_probe_mib > 0:
+            copy_probe(args.copy_probe_mib, torch.device("cuda:0"))
         return
     import workloads as W
 
@@ -259,14 +289,7 @@ def main():
                 "avg_launch_ms": round(avg_launch_ms, 5)}
 
     if args.copy_probe_mib > 0:
-        n = args.copy_probe_mib * (1 << 20)
-        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] copy probe: {args.copy_probe_mib} MiB device-to-device")
-        del src, dst
+        copy_probe(args.copy_probe_mib, dev)
 
     cpu = None
     if not args.no_cpu_baseline:

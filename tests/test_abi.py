@@ -174,6 +174,21 @@ def test_splitkv_workspace_size_and_validation():
     assert L.fabft_attn_fwd_splitkv(*args, 4, P, need - 1) == F.E_WORKSPACE
 
 
+def test_splitkv_default_splits():
+    """About 512 workgroups, at least 32 key tiles per split, 1..64 splits;
+    on the measured decode shapes the fastest count (or one within 1%)."""
+    assert F.splitkv_default_splits(4, 32, 1, 32768, 128) == 4
+    assert F.splitkv_default_splits(4, 32, 16, 32768, 128) == 4
+    assert F.splitkv_default_splits(1, 32, 1, 131072, 128) == 16
+    assert F.splitkv_default_splits(8, 8, 64, 8192, 128) == 4
+    for B, H, Lq, Lk, d in [(1, 1, 1, 64, 128), (1, 1, 1, 10 ** 6, 64), (64, 64, 4096, 4096, 128),
+                            (2, 3, 7, 777, 64), (1, 8, 1, 2 ** 20, 256)]:
+        ns = F.splitkv_default_splits(B, H, Lq, Lk, d)
+        tiles = -(-Lk // F.key_tile(d))
+        assert 1 <= ns <= 64
+        assert ns == 1 or tiles // ns >= 32
+
+
 def test_recompute_flagged_validation():
     L = F.lib()
     n1, n2 = ctypes.c_int(7), ctypes.c_int(7)
