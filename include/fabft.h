@@ -51,7 +51,10 @@ enum {
   FABFT_OK = 0,
   FABFT_E_NULL = -1,     /* a required pointer is NULL */
   FABFT_E_SHAPE = -2,    /* B, H, Lq or Lk < 1, or the grid is too large, or
-                            (Lk + 64) * d * 2 >= 2^32 */
+                            (Lk + 64) * d * 4 >= 2^32: one head's K or V
+                            (Lk * d * 2 bytes) and the reads past its end
+                            are addressed with 32-bit byte offsets (Lk at
+                            most 8388543 at d = 128) */
   FABFT_E_HEADDIM = -3,  /* d is not 64, 96, 128 or 256 */
   FABFT_E_ALIGN = -4,    /* q, k, v or o not 16-byte aligned */
   FABFT_E_LAUNCH = -5,   /* the kernel launch failed */

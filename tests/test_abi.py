@@ -73,6 +73,10 @@ def test_threshold_validation_and_roundtrip():
     ((P, P, P, P, P, P, 1, 1, 0, 8, 128, 0, 1.0), F.E_SHAPE),
     ((P, P, P, P, P, P, 1, 1, 8, -3, 128, 0, 1.0), F.E_SHAPE),
     ((P, P, P, P, P, P, 65536, 65536, 1024, 8, 128, 0, 1.0), F.E_SHAPE),
+    # a head's K/V byte offsets must fit 32 bits: (Lk + 64) * d * 4 <= 2^32 - 1
+    ((P, P, P, P, P, P, 1, 1, 1, 8388544, 128, 0, 1.0), F.E_SHAPE),   # first Lk past it
+    ((P, P, P, P, P, P, 1, 1, 1, 16777152, 64, 0, 1.0), F.E_SHAPE),
+    ((P, P, P, P, P, P, 1, 1, 1, 4194240, 256, 0, 1.0), F.E_SHAPE),
     ((P + 2, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_ALIGN),
     ((P, P, P + 8, P, P, P, 1, 1, 8, 8, 64, 0, 1.0), F.E_ALIGN),
     ((P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, -0.5), F.E_SCALE),
