@@ -213,10 +213,13 @@ struct Tile {
 
 // Rows of the small A operand that yields c and l: sumrow(V) as bf16 hi and
 // lo parts, ones, zeros, and the weighted row sums sum_j (-1)^j V_kj as hi
-// and lo parts, padded to 8 rows (1 KiB per key tile: one wave-wide 16-byte
-// load). MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9 read
-// WHi, WLo (accumulator elements 4, 5 of lanes 0-31); the others read the
-// zero row.
+// and lo parts, padded to 8 rows (one wave-wide 16-byte load per 16 keys).
+// MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9 read WHi, WLo
+// (accumulator elements 4, 5 of lanes 0-31); the others read the zero row.
+// Below d = 256 a row holds the tile's 64 keys plus 8 unused ones: with
+// 144-byte rows, rows 0-3 start 36 banks apart and one read touches no bank
+// twice (128-byte rows put rows 0 and 2, and 1 and 3, on the same banks). At
+// d = 256 (one wave per SIMD, no register to spare) the rows stay 128 bytes.
 enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRowWLo = 5,
        kVsmRows = 8 };
 
@@ -226,9 +229,10 @@ enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRow
 // d = 128, the reach of the LDS offset field).
 template <int D>
 struct Ring {
+  static constexpr int VS = D == 256 ? kBc : kBc + 8;   // vsm row stride (keys)
   uint16_t k[Cfg<D>::STAGES][kBc * D];
   uint16_t v[Cfg<D>::STAGES][kBc * D];
-  uint16_t vsm[Cfg<D>::STAGES][kVsmRows][kBc];
+  uint16_t vsm[Cfg<D>::STAGES][kVsmRows][VS];
 };
 
 template <int S>
@@ -407,12 +411,18 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     constexpr int CPT = CPR / TPK;       // 16-byte chunks per thread
     static_assert(TPK * BC == kThreads && CPT * TPK == CPR, "sumrow covers the tile");
     const uint16_t* const sv = ring.v[S];
-    uint16_t(*const svsm)[kBc] = ring.vsm[S];
+    uint16_t(*const svsm)[Ring<D>::VS] = ring.vsm[S];
     const int key = tid / TPK, part = tid % TPK;
     float a = 0.f, aw = 0.f;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      const u32x4 ch = *reinterpret_cast<const u32x4*>(&sv[Tile<D>::vidx(key, CPT * part + i)]);
+      // at d = 128: chunk part + 8 j, j = i ^ (key mod 2), so that the two
+      // keys of one 16-lane read pass (keys 2m, 2m+1) take opposite halves
+      // of the row, whose banks the V swizzle keeps apart (reading chunks
+      // 2 part + i put both keys on the same banks); every key still reads
+      // all of its chunks. Other widths read CPT consecutive chunks.
+      const int c = CPT == 2 ? part + TPK * (i ^ (key & 1)) : CPT * part + i;
+      const u32x4 ch = *reinterpret_cast<const u32x4*>(&sv[Tile<D>::vidx(key, c)]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         a = dot2(ch[e], kOnes, a);
@@ -441,7 +451,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     constexpr int S = decltype(S_)::value;
     const uint16_t* const sk = ring.k[S];
     const uint16_t* const sv = ring.v[S];
-    const uint16_t(*const svsm)[kBc] = ring.vsm[S];
+    const uint16_t(*const svsm)[Ring<D>::VS] = ring.vsm[S];
     const int kv0 = t * BC;
     const bool need_mask = (kv0 + BC > Lk) || (CAUSAL && kv0 + BC - 1 > wq_lo + off);
 
