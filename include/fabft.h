@@ -217,8 +217,8 @@ int fabft_get_weighted_check(void);
 int fabft_key_tile(int d);
 
 /* Number of query rows per workgroup for head dimension d (the unit of
- * fabft_fault.tile at the V and VS sites): 256, or 128 at d = 256;
- * FABFT_E_HEADDIM for an unsupported d. */
+ * fabft_fault.tile at the V and VS sites): 256 at d = 96 and 128, 128 at
+ * d = 64 and 256; FABFT_E_HEADDIM for an unsupported d. */
 int fabft_query_tile(int d);
 
 /* Fault sites for the injection path (where a single bit is flipped). */
