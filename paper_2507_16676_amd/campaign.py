@@ -318,10 +318,11 @@ def summarize(path):
             "paper_table_by_nfaults": {k: paper_table(v) for k, v in sorted(by_k.items())}}
 
 
-def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000):
+def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000, score_check=False):
     """Fault-free runs on seeds seed0..seed0+seeds-1: count flagged rows
     (must be 0) and track rho = max |resid| / (sum_j |O_ij| + |pred|), and
-    with the weighted check on, the same ratio for it (rho_w)."""
+    with the weighted check on, the same ratio for it (rho_w). score_check
+    records that the caller switched the score check on (its flags count)."""
     torch = _torch()
     from . import attn_fwd, attn_fwd_inject, get_threshold, get_weighted_check
     weighted = get_weighted_check()
@@ -357,7 +358,8 @@ def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000):
     res = {"workload": w.name, "seeds": seeds, "seed0": seed0, "rows_checked": rows,
            "flagged_rows": flagged_total, "flagged_seeds": flagged_seeds[:100],
            "rho_max": rho_max, "rho_seeds": rho_seeds, "threshold": get_threshold(),
-           "weighted_check": weighted, "seconds": time.time() - t0}
+           "weighted_check": weighted, "score_check": bool(score_check),
+           "seconds": time.time() - t0}
     if weighted:
         res["rho_w_max"] = rho_w_max
     if out_path:
@@ -398,6 +400,8 @@ def main(argv=None):
     s.add_argument("--out", required=True)
     s.add_argument("--weighted", action="store_true",
                    help="also run the weighted (alternating-sign) checksum")
+    s.add_argument("--score-check", action="store_true",
+                   help="also run the score check (row sums of Q K^T); its flags count too")
     a = ap.parse_args(argv)
     w = W.WORKLOADS[a.workload]
     if a.weighted:
@@ -432,7 +436,14 @@ def main(argv=None):
                           "false_positives": summ["false_positives"],
                           "paper_table": summ["paper_table"]}))
     else:
-        print(json.dumps(run_sweep(w, a.seeds, a.out, seed0=a.seed0, rho_every=a.rho_every)))
+        if a.score_check:
+            import torch
+            from . import score_check_workspace_bytes, set_score_check
+            ws = torch.empty(score_check_workspace_bytes(w.B, w.H, w.Lk, w.d), dtype=torch.uint8,
+                             device="cuda")
+            set_score_check(ws)
+        print(json.dumps(run_sweep(w, a.seeds, a.out, seed0=a.seed0, rho_every=a.rho_every,
+                                   score_check=a.score_check)))
 
 
 if __name__ == "__main__":
