@@ -284,7 +284,8 @@ def main():
     roofline = {"bound": "mfma", "achieved": round(achieved, 2),
                 "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
-                "kernel": (f"fabft::fwd_kernel<{w.d}, {str(w.causal).lower()}, true, false, "
+                "kernel": (f"fabft::fwd_kernel<{128 if w.d == 96 else w.d}, "
+                           f"{str(w.causal).lower()}, true, false, "
                            f"false, false, false>"),
                 "avg_launch_ms": round(avg_launch_ms, 5)}
 
