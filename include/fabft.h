@@ -125,6 +125,31 @@ int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v,
                            float scale, int nsplit, void* workspace,
                            long long workspace_bytes);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * fabft_attn_fwd_splitkv with its per-split partial states kept in a buffer
+ * that the library owns instead of a caller workspace. The buffer is a static
+ * device array of FABFT_NOALLOC_SCRATCH_BYTES bytes (64 MiB), one copy per
+ * GPU, held by every GPU the library runs on until the process ends; its
+ * device address is looked up once per GPU, on the first call whose stream
+ * belongs to that GPU. Arguments, results and validation as in
+ * fabft_attn_fwd_splitkv; a problem whose workspace need
+ * (fabft_splitkv_workspace_bytes) exceeds FABFT_NOALLOC_SCRATCH_BYTES returns
+ * FABFT_E_WORKSPACE before anything is launched. The call allocates nothing
+ * (no hipMalloc, hipFree or allocating library routine). Every call on one
+ * GPU shares that GPU's buffer and leaves the last call's partial states in
+ * it: calls that overlap on one GPU (other streams, other host threads)
+ * race and must be serialised by the caller. Nothing in the buffer needs to
+ * start at zero (every record the merge reads is written by the same call).
+ * Asynchronous (two launches in order on the library stream).
+ */
+#define FABFT_NOALLOC_SCRATCH_BYTES (64LL << 20)
+int fabft_attn_fwd_splitkv_noalloc(const void* q, const void* k, const void* v,
+                                   void* o, float* resid, uint8_t* flags,
+                                   int B, int H, int Lq, int Lk, int d,
+                                   int causal, float scale, int nsplit);
+
 /* Stream for all subsequent launches (a hipStream_t; NULL = null stream). */
 void fabft_set_stream(void* hip_stream);
 

@@ -86,6 +86,9 @@ def _load() -> ctypes.CDLL:
     L.fabft_attn_fwd_splitkv.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                          _f, _i, _vp, ctypes.c_longlong]
     L.fabft_attn_fwd_splitkv.restype = _i
+    L.fabft_attn_fwd_splitkv_noalloc.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i,
+                                                 _i, _i, _f, _i]
+    L.fabft_attn_fwd_splitkv_noalloc.restype = _i
     L.fabft_recompute_flagged.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                           _f, _vp, _vp, _i, ctypes.POINTER(_i),
                                           ctypes.POINTER(_i)]
@@ -110,6 +113,7 @@ EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
            "fabft_attn_fwd_inject_n", "fabft_score_check_workspace_bytes",
            "fabft_set_score_check", "fabft_get_score_threshold",
            "fabft_attn_fwd_splitkv", "fabft_splitkv_workspace_bytes",
+           "fabft_attn_fwd_splitkv_noalloc",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
            "fabft_global_check", "fabft_recompute_flagged",
            "fabft_set_weighted_check", "fabft_get_weighted_check",

@@ -7,11 +7,19 @@
 #include <climits>
 #include <cmath>
 #include <cstdint>
+#include <mutex>
 
 #include "../../include/fabft.h"
 #include "fabft_kernels.h"
 
 static_assert(FABFT_MAX_FAULTS == fabft::kMaxFaults, "fault list size");
+
+// Library-owned scratch of the allocation-free key split: one copy per GPU,
+// held from the library's load until the process ends. In host code the
+// array's name is only a stand-in for the symbol; the device address of
+// each GPU's copy comes from hipGetSymbolAddress with that GPU current, once
+// per device, and is the only form ever passed to a kernel.
+static __device__ __align__(256) unsigned char scratch[FABFT_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -151,6 +159,49 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
 
 namespace {
 
+// The key split (SPLIT kernels, then the merge) on a validated problem with a
+// workspace of at least fabft_splitkv_workspace_bytes bytes.
+int launch_splitkv(const void* q, const void* k, const void* v, void* o, float* resid,
+                   uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal, float scale,
+                   int n_qt, int grid, int nsplit, void* workspace) {
+  const long long g = static_cast<long long>(grid) * nsplit;
+  if (g > INT_MAX) return FABFT_E_SHAPE;
+  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid);
+  const int bc = fabft::key_tile(d);
+  const int tiles = (Lk + bc - 1) / bc;
+  p.nsplit = nsplit;
+  p.split_tiles = (tiles + nsplit - 1) / nsplit;
+  p.ws = static_cast<float*>(workspace);
+  p.grid = static_cast<int>(g);
+  if (fabft::launch_fwd(p, d, causal != 0, 3, g_stream) != 0) return FABFT_E_LAUNCH;
+  return fabft::launch_merge(p, d, B * H, g_stream) == 0 ? FABFT_OK : FABFT_E_LAUNCH;
+}
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of `scratch` on the device that `stream` belongs to
+// (looked up on that device's first call).
+int scratch_for_stream(hipStream_t stream, void** out) {
+  hipDevice_t dev = 0;
+  if (hipStreamGetDevice(stream, &dev) != hipSuccess) return FABFT_E_LAUNCH;
+  if (dev < 0 || dev >= kMaxDevices) return FABFT_E_LAUNCH;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    int cur = 0;
+    if (hipGetDevice(&cur) != hipSuccess) return FABFT_E_LAUNCH;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return FABFT_E_LAUNCH;
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !ptr) return FABFT_E_LAUNCH;
+    g_scratch_ptr[dev] = ptr;
+  }
+  *out = g_scratch_ptr[dev];
+  return FABFT_OK;
+}
+
 // Range checks of one fault descriptor against the problem (site semantics in
 // include/fabft.h).
 int check_fault(const fabft_fault* f, int B, int H, int Lq, int Lk, int d, int causal, int n_qt) {
@@ -264,19 +315,26 @@ int fabft_attn_fwd_splitkv(const void* q, const void* k, const void* v, void* o,
   const long long need = fabft_splitkv_workspace_bytes(B, H, Lq, d, nsplit);
   if (need < 0) return static_cast<int>(need);
   if (workspace_bytes < need) return FABFT_E_WORKSPACE;
-  const long long g = static_cast<long long>(grid) * nsplit;
-  if (g > INT_MAX) return FABFT_E_SHAPE;
-  fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid);
-  const int bc = fabft::key_tile(d);
-  const int tiles = (Lk + bc - 1) / bc;
-  p.nsplit = nsplit;
-  p.split_tiles = (tiles + nsplit - 1) / nsplit;
-  p.ws = static_cast<float*>(workspace);
-  p.grid = static_cast<int>(g);
-  rc = fabft::launch_fwd(p, d, causal != 0, 3, g_stream);
-  if (rc != 0) return FABFT_E_LAUNCH;
-  rc = fabft::launch_merge(p, d, B * H, g_stream);
-  return rc == 0 ? FABFT_OK : FABFT_E_LAUNCH;
+  return launch_splitkv(q, k, v, o, resid, flags, B, H, Lq, Lk, d, causal, scale, n_qt, grid,
+                        nsplit, workspace);
+}
+
+int fabft_attn_fwd_splitkv_noalloc(const void* q, const void* k, const void* v, void* o,
+                                   float* resid, uint8_t* flags, int B, int H, int Lq, int Lk,
+                                   int d, int causal, float scale, int nsplit) {
+  int n_qt = 0, grid = 0;
+  int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
+  if (rc != FABFT_OK) return rc;
+  if (!resid || !flags) return FABFT_E_NULL;
+  if (nsplit < 1 || nsplit > kMaxSplits) return FABFT_E_SHAPE;
+  const long long need = fabft_splitkv_workspace_bytes(B, H, Lq, d, nsplit);
+  if (need < 0) return static_cast<int>(need);
+  if (need > FABFT_NOALLOC_SCRATCH_BYTES) return FABFT_E_WORKSPACE;
+  void* ws = nullptr;
+  rc = scratch_for_stream(g_stream, &ws);
+  if (rc != FABFT_OK) return rc;
+  return launch_splitkv(q, k, v, o, resid, flags, B, H, Lq, Lk, d, causal, scale, n_qt, grid,
+                        nsplit, ws);
 }
 
 int fabft_recompute_flagged(const void* q, const void* k, const void* v, void* o, float* resid,

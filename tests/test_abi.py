@@ -178,6 +178,29 @@ def test_splitkv_workspace_size_and_validation():
     assert L.fabft_attn_fwd_splitkv(*args, 4, P, need - 1) == F.E_WORKSPACE
 
 
+def test_splitkv_noalloc_validation():
+    """The allocation-free key split validates like the workspace form and
+    rejects a problem whose partial states exceed its static buffer before
+    anything touches the GPU."""
+    L = F.lib()
+    args = (P, P, P, P, P, P, 1, 2, 8, 8, 128, 1, 0.1)
+    assert L.fabft_attn_fwd_splitkv_noalloc(*args[:4], None, P, *args[6:], 4) == F.E_NULL
+    assert L.fabft_attn_fwd_splitkv_noalloc(*args[:5], None, *args[6:], 4) == F.E_NULL
+    assert L.fabft_attn_fwd_splitkv_noalloc(*args, 0) == F.E_SHAPE
+    assert L.fabft_attn_fwd_splitkv_noalloc(*args, 65) == F.E_SHAPE
+    bad_d = args[:10] + (80,) + args[11:]
+    assert L.fabft_attn_fwd_splitkv_noalloc(*bad_d, 4) == F.E_HEADDIM
+    # 1 * 1024 heads * 1024 rows * (128 + 4) floats: 528 MiB > 64 MiB
+    big = (P, P, P, P, P, P, 1, 1024, 1024, 64, 128, 0, 0.1)
+    assert L.fabft_splitkv_workspace_bytes(1, 1024, 1024, 128, 1) > (64 << 20)
+    assert L.fabft_attn_fwd_splitkv_noalloc(*big, 1) == F.E_WORKSPACE
+    # the largest accepted problem fits exactly: (d + 4) * 4 bytes per row
+    # and split, 64 MiB = 127100 rows at d = 128 with one split (not run)
+    rows = (64 << 20) // ((128 + 4) * 4)
+    assert L.fabft_splitkv_workspace_bytes(1, 1, rows, 128, 1) <= (64 << 20)
+    assert L.fabft_splitkv_workspace_bytes(1, 1, rows + 1, 128, 1) > (64 << 20)
+
+
 def test_splitkv_default_splits():
     """About 512 workgroups, at least 32 key tiles per split, 1..64 splits;
     on the measured decode shapes the fastest count (or one within 1%)."""
