@@ -39,9 +39,9 @@ x is the kernel's own state. The fault model fixes it (the same description
 the library's header gives for each site):
   * scores in exp2 units u_k = s_k * sl2 with sl2 = scale * log2(e) in fp32;
   * keys come in tiles of `key_tile`; after the max of tile t the exponent
-    reference moves to the tile max only when it exceeds the reference by
-    more than 8 (lazy rescaling), and the weights of tile t are
-    p~_k = bf16(2^(u_k - ref_t)) (round to nearest even);
+    reference moves to the tile max (rounded to fp32) only when it exceeds
+    the reference by more than 8 (lazy rescaling), and the weights of tile t
+    are p~_k = bf16(2^(u_k - ref_t)) (round to nearest even);
   * after tile t, o, l and c sit in the frame of ref_t:
     o_j(t) = sum_{k <= end of t} p~_k 2^(ref_{t(k)} - ref_t) V_kj, and l, c
     alike with 1 and the sumrow parts;
@@ -184,7 +184,8 @@ def row_frame(s: np.ndarray, vis: np.ndarray, sl2: float, v: np.ndarray,
     for t in range(nt):
         a, b = t * key_tile, min(Lk, (t + 1) * key_tile)
         vt = vis[a:b]
-        mt = u[a:b][vt].max() if vt.any() else -np.inf
+        # the tile max enters the reference as an fp32 product
+        mt = float(np.float32(u[a:b][vt].max())) if vt.any() else -np.inf
         new = mt if mt > ref + LAZY else ref
         if np.isfinite(ref) and new != ref:
             alpha = 2.0 ** (ref - new)
@@ -229,7 +230,7 @@ def _wave_sees_tile(i: int, t: int, Lq: int, Lk: int, causal: bool, key_tile: in
 # --------------------------------------------------------------------------
 
 def _row_result(O, pred, dO, dpred, tau_rel, tau_abs, nonfinite=False, nonfinite_maybe=False,
-                O_new=None, pred_new=None, err_o=None, err_p=0.0):
+                O_new=None, pred_new=None, err_o=None, err_p=0.0, undetermined=False):
     """Residual, threshold and flag of one row after a fault. err_o [d] and
     err_p bound what the bf16 rounding of the kernel's weights can move dO
     and dpred by, in units of 2^-8 (each weight and l carry a relative
@@ -255,7 +256,7 @@ def _row_result(O, pred, dO, dpred, tau_rel, tau_abs, nonfinite=False, nonfinite
             "dactual": actual_new - actual, "resid": r, "M": M, "flag": flag,
             "nonfinite": nonfinite, "nonfinite_maybe": bool(nonfinite_maybe),
             "significant": sig, "dO_err": err_o, "dpred_err": float(err_p),
-            "dactual_err": float(err_o.sum())}
+            "dactual_err": float(err_o.sum()), "undetermined": bool(undetermined)}
 
 
 def bf16_max() -> float:
@@ -361,8 +362,10 @@ def fault_effect(q, k, v, causal: bool, scale: float, fault: FaultSpec, key_tile
             den = float(P[e:].sum()) + (xn / x) * float(P[:e].sum()) if np.isfinite(xn) else np.inf
             if not (den > 0.0) or not np.isfinite(den):
                 # l' not positive or not finite: the kernel writes O = 0, pred = 0
+                # (the change is -O: the rounding of O's own weights bounds it)
                 res = _row_result(O, pred, None, None, tau_rel, tau_abs,
-                                  O_new=np.zeros_like(O), pred_new=0.0)
+                                  O_new=np.zeros_like(O), pred_new=0.0,
+                                  err_o=P @ np.abs(v), err_p=float(P @ np.abs(vs)))
             else:
                 # O' = O / den: the rounding of every weight enters, scaled
                 res = _row_result(O, pred, None, None, tau_rel, tau_abs, O_new=O / den,
@@ -383,10 +386,15 @@ def fault_effect(q, k, v, causal: bool, scale: float, fault: FaultSpec, key_tile
                                   nonfinite=True)
             else:
                 Pn = _softmax_row(s_new, vis, scale)
+                # a new row max beyond 2^30 in exp2 units: the kernel's weight
+                # of that key is 2 to the fp32 rounding residual of its score
+                # times sl2 (up to 2^6 and more), which depends on score bits
+                # below fp64's view of them; the outcome is not determined here
+                und = bool(np.max(s_new[vis]) * sl2 >= 2.0 ** 30)
                 # every weight changes: both rows' rounding enters
                 res = _row_result(O, pred, None, None, tau_rel, tau_abs, O_new=Pn @ v,
                                   pred_new=float(Pn @ vs), err_o=(P + Pn) @ np.abs(v),
-                                  err_p=float((P + Pn) @ np.abs(vs)))
+                                  err_p=float((P + Pn) @ np.abs(vs)), undetermined=und)
         return _summary([i], [res])
 
     if site in ("V", "VS"):
@@ -433,6 +441,7 @@ def fault_effect(q, k, v, causal: bool, scale: float, fault: FaultSpec, key_tile
 
 def _summary(rows, res):
     return {"rows": list(rows), "per_row": res,
+            "undetermined": any(r["undetermined"] for r in res),
             "flagged": any(r["flag"] for r in res),
             "significant": any(r["significant"] for r in res),
             "nonfinite": any(r["nonfinite"] for r in res),

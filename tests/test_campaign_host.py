@@ -89,6 +89,18 @@ def test_classify_outcomes():
     fl2 = none.clone()
     fl2[2] = 1
     assert C.classify(tiny, g, fl2)["outcome"] == "detected_minor"
+    # one bf16 unit at the row's largest element exceeds 2^-8 of it: a
+    # rounding step alone is not significant, two units past the level are
+    big = g.clone()
+    j = int(big[4].float().abs().argmax())
+    one_up = (big[4, j].float() + C.bf16_unit(big[4, j:j + 1])[0] * torch.sign(big[4, j].float()))
+    big[4, j] = one_up.to(torch.bfloat16)
+    assert float((big[4, j].float() - g[4, j].float()).abs()) > 2 ** -8 * float(g[4].float().abs().max())
+    assert C.classify(big, g, none)["outcome"] == "benign"
+    big[4, j] = (g[4, j].float() * (1 + 2 ** -5)).to(torch.bfloat16)
+    assert C.classify(big, g, none)["outcome"] == "silent"
+    u = C.bf16_unit(torch.tensor([1.0, 1.5, -3.0, 0.0, 2.0 ** -126, 2.0 ** -130]).to(torch.bfloat16))
+    assert u.tolist() == [2.0 ** -7, 2.0 ** -7, 2.0 ** -6, 0.0, 2.0 ** -133, 2.0 ** -133]
     nan = g.clone()
     nan[1, 1] = float("nan")
     res = C.classify(nan, g, none)

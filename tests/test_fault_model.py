@@ -95,6 +95,8 @@ def brute(q, k, v, causal, scale, fault, key_tile, query_tile, exact=False, fact
                     sc = sc * factor if exact else f32_flip(f32(sc), fault.bit)
                 s[kk] = sc
             mt = max((s[kk] * sl2 for kk in s), default=-math.inf)
+            if not exact and mt != -math.inf:
+                mt = f32(mt)
             new = mt if mt > ref + FM.LAZY else ref
             if new != ref and ref != -math.inf:
                 a = 2.0 ** (ref - new)
@@ -241,7 +243,7 @@ def test_prediction_matches_brute_force(n, causal, Lq, Lk, d, site, bit):
         if res["nonfinite"]:
             assert bad, (i, O1, p1)
             continue
-        if res["nonfinite_maybe"]:
+        if res["nonfinite_maybe"] or res["undetermined"]:
             continue
         assert not bad, (i, res)
         dO_b = np.array(O1) - np.array(O0)
