@@ -327,6 +327,44 @@ int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v,
                             float* pred, float* actual,
                             float* pred_w, float* actual_w);
 
+/*
+ * Optional per-row debug outputs of fabft_attn_fwd_debug; each pointer may be
+ * NULL (not written), else fp32 [B, H, Lq] on the device.
+ *  pred, actual      c / l (Eq. 8) and sum_j O_ij (fp32, before rounding)
+ *  pred_w, actual_w  the weighted check's c_w / l and sum_j (-1)^j O_ij
+ *                    (0 while the weighted check is off)
+ *  score_lhs         the score check's sum of the row's raw scores q_i . k_k
+ *                    over the key tiles without a mask (see
+ *                    fabft_set_score_check), as they entered the softmax
+ *  score_rhs         q_i . sum_k K_k over the same keys (the q_i held at the
+ *                    end of the pass)
+ *  score_bound       |q_i| . sum_k |K_k| over the same keys (the threshold is
+ *                    tau_s times it)
+ * The three score outputs are 0 while the score check is off. Section II's
+ * row checksum of a matrix product, applied to S = Q K^T.
+ */
+typedef struct {
+  float* pred;
+  float* actual;
+  float* pred_w;
+  float* actual_w;
+  float* score_lhs;
+  float* score_rhs;
+  float* score_bound;
+} fabft_debug_out;
+
+/*
+ * Debug / fault-injection forward with every debug output: the same
+ * computation and fault list as fabft_attn_fwd_inject_n (the injection
+ * instantiation), writing the outputs `out` selects (out may be NULL).
+ * Asynchronous.
+ */
+int fabft_attn_fwd_debug(const void* q, const void* k, const void* v,
+                         void* o, float* resid, uint8_t* flags,
+                         int B, int H, int Lq, int Lk, int d, int causal,
+                         float scale, const fabft_fault* faults, int nfaults,
+                         const fabft_debug_out* out);
+
 /* Human-readable text for a status code (static storage). */
 const char* fabft_status_str(int status);
 

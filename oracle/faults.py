@@ -69,7 +69,7 @@ import numpy as np
 
 __all__ = ["FaultSpec", "LAZY", "SIG_REL", "bf16_round_bits", "bf16_bits_value",
            "flip_bf16", "flip_f32", "exp2_scale", "row_frame", "fault_effect",
-           "score_check_row", "classify_prediction"]
+           "score_check_row", "score_check_fault", "classify_prediction"]
 
 LAZY = 8.0                 # reference moves when a tile max exceeds it by more than this
 SIG_REL = 2.0 ** -8        # significance of an output change (campaign classification)
@@ -483,3 +483,53 @@ def score_check_row(q, k, i: int, Lq: int, causal: bool, key_tile: int = 64) -> 
     ks = k[:n]
     return {"lhs": float((ks @ q[i]).sum()), "rhs": float(q[i] @ ks.sum(axis=0)),
             "ms": float(np.abs(q[i]) @ np.abs(ks).sum(axis=0)), "n": n}
+
+
+def score_check_fault(q, k, i: int, Lq: int, causal: bool, fault: FaultSpec,
+                      key_tile: int = 64, tau_s: float = 2.0 ** -22, tau_abs: float = 0.0) -> dict:
+    """The score check of row i after an S or Q fault (other sites leave it
+    as score_check_row gives it). S (row i, key k): the flipped fp32 score
+    enters lhs if k lies in the full tiles; the right-hand side is unchanged.
+    Q (row i, column j, from key tile t on): the scores of tiles >= t use the
+    flipped q_ij, and rhs and the bound use it for every full tile (the q
+    the row holds at the end). Returns lhs, rhs, ms, n, flag (the score
+    flag: |lhs - rhs| > tau_s * ms + tau_abs with finite sums), nonfinite
+    (the sums are not finite: the row counts as non-finite instead), term
+    (the magnitude of the changed terms, sum of |x_j y_j| scaled by the flip,
+    which bounds what fp32 rounding of the kernel's scores can move) and
+    undetermined (a sum beyond 2^100: fp32 overflow inside the kernel's sums
+    decides the outcome)."""
+    q = np.asarray(q, dtype=np.float64)
+    k = np.asarray(k, dtype=np.float64)
+    r = score_check_row(q, k, i, Lq, causal, key_tile)
+    n = r["n"]
+    lhs, rhs, ms = r["lhs"], r["rhs"], r["ms"]
+    term = 0.0   # scale of the changed terms: the kernel's fp32 score carries
+    # a rounding of order 2^-24 of sum_j |q_ij k_kj|, which a flip scales by f
+    if fault.row == i and fault.site == "S" and fault.col < n:
+        s = float(k[fault.col] @ q[i])
+        sn = flip_f32(s, fault.bit)
+        lhs = lhs + sn - float(np.float32(s))
+        s32 = float(np.float32(s))
+        f = abs(sn / s32) if s32 != 0.0 else abs(sn)
+        term = f * float(np.abs(k[fault.col]) @ np.abs(q[i]))
+    elif fault.row == i and fault.site == "Q":
+        j = fault.col
+        qn = q[i].copy()
+        qn[j] = flip_bf16(q[i, j], fault.bit)
+        a = min(n, fault.tile * key_tile)
+        ks = k[:n]
+        with np.errstate(invalid="ignore", over="ignore"):
+            lhs = float((ks[:a] @ q[i]).sum() + (ks[a:] @ qn).sum())
+            rhs = float(qn @ ks.sum(axis=0))
+            ms = float(np.abs(qn) @ np.abs(ks).sum(axis=0))
+            term = float(abs(qn[j] - q[i, j]) * np.abs(ks[:, j]).sum())
+    with np.errstate(invalid="ignore"):
+        d = lhs - rhs
+        nonfinite = bool(not np.isfinite(d) or not np.isfinite(ms))
+        flag = bool(not nonfinite and abs(d) > tau_s * ms + tau_abs)
+        # sums near the fp32 range: whether the kernel's fp32 products and
+        # sums overflow (and in which order) decides the outcome
+        und = bool(not nonfinite and max(abs(lhs), abs(rhs), ms, term) > 2.0 ** 100)
+    return {"lhs": lhs, "rhs": rhs, "ms": ms, "n": n, "flag": flag, "nonfinite": nonfinite,
+            "term": term, "undetermined": und}

@@ -10,7 +10,9 @@ built, every call raises.
     o = attn_fwd(q, k, v, causal=True, check=False)         # checksum off
 
 q: [B, H, Lq, d], k and v: [B, H, Lk, d], torch.bfloat16 on the GPU,
-contiguous; d in {64, 128}. scale defaults to 1/sqrt(d).
+contiguous; d in {64, 96, 128, 256}. scale defaults to 1/sqrt(d). Every
+caller-supplied tensor (out=, workspaces) is checked for shape, dtype,
+contiguity and device before the library sees its pointer.
 """
 from __future__ import annotations
 
@@ -38,6 +40,11 @@ MAX_FAULTS = 8
 class FabftFault(ctypes.Structure):
     _fields_ = [("site", _i), ("b", _i), ("h", _i), ("row", _i), ("col", _i),
                 ("tile", _i), ("bit", _i)]
+
+
+class FabftDebugOut(ctypes.Structure):
+    _fields_ = [("pred", _vp), ("actual", _vp), ("pred_w", _vp), ("actual_w", _vp),
+                ("score_lhs", _vp), ("score_rhs", _vp), ("score_bound", _vp)]
 
 
 _LIB = None
@@ -69,6 +76,10 @@ def _load() -> ctypes.CDLL:
                                           _f, ctypes.POINTER(FabftFault), _i, _vp, _vp, _vp,
                                           _vp]
     L.fabft_attn_fwd_inject_n.restype = _i
+    L.fabft_attn_fwd_debug.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
+                                       _f, ctypes.POINTER(FabftFault), _i,
+                                       ctypes.POINTER(FabftDebugOut)]
+    L.fabft_attn_fwd_debug.restype = _i
     L.fabft_score_check_workspace_bytes.argtypes = [_i, _i, _i, _i]
     L.fabft_score_check_workspace_bytes.restype = ctypes.c_longlong
     L.fabft_set_score_check.argtypes = [_vp, ctypes.c_longlong, _f]
@@ -110,7 +121,7 @@ def _load() -> ctypes.CDLL:
 
 
 EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
-           "fabft_attn_fwd_inject_n", "fabft_score_check_workspace_bytes",
+           "fabft_attn_fwd_inject_n", "fabft_attn_fwd_debug", "fabft_score_check_workspace_bytes",
            "fabft_set_score_check", "fabft_get_score_threshold",
            "fabft_attn_fwd_splitkv", "fabft_splitkv_workspace_bytes",
            "fabft_attn_fwd_splitkv_noalloc",
@@ -167,6 +178,10 @@ def set_score_check(workspace=None, tau_s: float = 0.0):
         _check(_load().fabft_set_score_check(None, 0, 0.0), "fabft_set_score_check")
         _SCORE_WS = None
         return
+    import torch
+    if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda or \
+            not workspace.is_contiguous():
+        raise ValueError("the score-check workspace must be a contiguous GPU tensor")
     nbytes = workspace.numel() * workspace.element_size()
     _check(_load().fabft_set_score_check(workspace.data_ptr(), nbytes, float(tau_s)),
            "fabft_set_score_check")
@@ -214,6 +229,35 @@ def _shape(q, k, v):
     return B, H, Lq, k.shape[2], d
 
 
+def _check_out(t, name: str, shape, dtype, device):
+    """A caller-supplied tensor must have exactly this shape and dtype, be
+    contiguous and sit on `device`: the library only sees its pointer and
+    would write past the end of a short or mistyped buffer."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if tuple(t.shape) != tuple(shape) or t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype} of shape {tuple(shape)}, got {t.dtype} "
+                         f"{tuple(t.shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.device != device:
+        raise ValueError(f"{name} must be on {device}, got {t.device}")
+    return t
+
+
+def _check_workspace(t, name: str, need: int, device):
+    """A workspace: a contiguous tensor on `device` of at least `need` bytes."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch tensor")
+    if not t.is_contiguous() or t.device != device:
+        raise ValueError(f"{name} must be a contiguous tensor on {device}")
+    if t.numel() * t.element_size() < need:
+        raise ValueError(f"{name} holds {t.numel() * t.element_size()} bytes, {need} needed")
+    return t
+
+
 def _stream(dev):
     import torch
     _load().fabft_set_stream(ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream))
@@ -230,7 +274,9 @@ def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, check: b
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
     dev = q.device
     if out is not None:
-        o = out[0]
+        if len(out) not in (1, 3) or (check and len(out) != 3):
+            raise ValueError("out must be (o,) with check=False, or (o, resid, flags)")
+        o = _check_out(out[0], "out[0] (o)", q.shape, torch.bfloat16, dev)
     else:
         o = torch.empty_like(q)
     _stream(dev)
@@ -239,8 +285,9 @@ def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, check: b
                                            B, H, Lq, Lk, d, int(bool(causal)), scale),
                "fabft_attn_fwd_nocheck")
         return o
-    if out is not None and len(out) == 3:
-        resid, flags = out[1], out[2]
+    if out is not None:
+        resid = _check_out(out[1], "out[1] (resid)", (B, H, Lq), torch.float32, dev)
+        flags = _check_out(out[2], "out[2] (flags)", (B, H, Lq), torch.uint8, dev)
     else:
         resid = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
         flags = torch.empty((B, H, Lq), dtype=torch.uint8, device=dev)
@@ -282,8 +329,12 @@ def attn_fwd_splitkv(q, k, v, causal: bool = False, scale: float | None = None,
     need = splitkv_workspace_bytes(B, H, Lq, d, nsplit)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=dev)
+    _check_workspace(workspace, "workspace", need, dev)
     if out is not None:
         o, resid, flags = out
+        _check_out(o, "out[0] (o)", q.shape, torch.bfloat16, dev)
+        _check_out(resid, "out[1] (resid)", (B, H, Lq), torch.float32, dev)
+        _check_out(flags, "out[2] (flags)", (B, H, Lq), torch.uint8, dev)
     else:
         o = torch.empty_like(q)
         resid = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
@@ -292,7 +343,8 @@ def attn_fwd_splitkv(q, k, v, causal: bool = False, scale: float | None = None,
     _check(_load().fabft_attn_fwd_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                                           resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
                                           int(bool(causal)), scale, int(nsplit),
-                                          workspace.data_ptr(), workspace.numel()),
+                                          workspace.data_ptr(),
+                                          workspace.numel() * workspace.element_size()),
            "fabft_attn_fwd_splitkv")
     return o, resid, flags
 
@@ -305,6 +357,9 @@ def recompute_flagged(q, k, v, o, resid, flags, causal: bool = False,
     import torch
     B, H, Lq, Lk, d = _shape(q, k, v)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    _check_out(o, "o", q.shape, torch.bfloat16, q.device)
+    _check_out(resid, "resid", (B, H, Lq), torch.float32, q.device)
+    _check_out(flags, "flags", (B, H, Lq), torch.uint8, q.device)
     hf = torch.empty(B * H, dtype=torch.uint8, device=q.device)
     hf_host = np.zeros(B * H, dtype=np.uint8)
     nr, npers = ctypes.c_int(), ctypes.c_int()
@@ -326,8 +381,7 @@ def global_check(o, resid):
     if o.dtype != torch.bfloat16 or not o.is_cuda or not o.is_contiguous() or o.dim() != 4:
         raise ValueError("o must be a contiguous bf16 [B, H, Lq, d] GPU tensor")
     B, H, Lq, d = o.shape
-    if tuple(resid.shape) != (B, H, Lq) or resid.dtype != torch.float32 or not resid.is_contiguous():
-        raise ValueError("resid must be a contiguous fp32 [B, H, Lq] tensor")
+    _check_out(resid, "resid", (B, H, Lq), torch.float32, o.device)
     gsum = torch.empty((B, H), dtype=torch.float64, device=o.device)
     gflags = torch.empty((B, H), dtype=torch.uint8, device=o.device)
     _stream(o.device)
@@ -352,11 +406,48 @@ class Fault:
                           self.bit)
 
 
+def _faults_array(fault):
+    faults = [] if fault is None else ([fault] if isinstance(fault, Fault) else list(fault))
+    if len(faults) > MAX_FAULTS:
+        raise ValueError(f"at most {MAX_FAULTS} faults per launch")
+    return (FabftFault * max(1, len(faults)))(*[f.to_c() for f in faults]), len(faults)
+
+
+def attn_fwd_debug(q, k, v, causal: bool = False, scale: float | None = None, fault=None,
+                   outputs=("pred", "actual", "pred_w", "actual_w", "score_lhs",
+                            "score_rhs", "score_bound")):
+    """Debug / fault-injection forward with the debug outputs named in
+    `outputs` (see fabft_debug_out). Returns a dict with o, resid, flags and
+    one fp32 [B, H, Lq] tensor per requested output."""
+    import torch
+    B, H, Lq, Lk, d = _shape(q, k, v)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dev = q.device
+    res = {"o": torch.empty_like(q),
+           "resid": torch.empty((B, H, Lq), dtype=torch.float32, device=dev),
+           "flags": torch.empty((B, H, Lq), dtype=torch.uint8, device=dev)}
+    dbg = FabftDebugOut()
+    for name in outputs:
+        if name not in dict(FabftDebugOut._fields_):
+            raise ValueError(f"unknown debug output {name!r}")
+        res[name] = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+        setattr(dbg, name, res[name].data_ptr())
+    arr, n = _faults_array(fault)
+    _stream(dev)
+    _check(_load().fabft_attn_fwd_debug(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                        res["o"].data_ptr(), res["resid"].data_ptr(),
+                                        res["flags"].data_ptr(), B, H, Lq, Lk, d,
+                                        int(bool(causal)), scale, arr, n, ctypes.byref(dbg)),
+           "fabft_attn_fwd_debug")
+    return res
+
+
 def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
                     fault=None, out=None, weighted_out: bool = False):
     """Debug / fault-injection forward. fault: None, one Fault, or a list of
     up to MAX_FAULTS Faults applied in the same launch. Returns (o, resid,
-    flags, pred, actual), followed by (pred_w, actual_w) with weighted_out=True."""
+    flags, pred, actual), followed by (pred_w, actual_w) with weighted_out=True.
+    out: optional preallocated (o, resid, flags, pred, actual)."""
     import torch
     B, H, Lq, Lk, d = _shape(q, k, v)
     scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
@@ -368,17 +459,23 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
         pred = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
         actual = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
     else:
-        o, resid, flags, pred, actual = out[:5]
+        if len(out) != 5:
+            raise ValueError("out must be (o, resid, flags, pred, actual)")
+        o, resid, flags, pred, actual = out
+        _check_out(o, "out[0] (o)", q.shape, torch.bfloat16, dev)
+        _check_out(resid, "out[1] (resid)", (B, H, Lq), torch.float32, dev)
+        _check_out(flags, "out[2] (flags)", (B, H, Lq), torch.uint8, dev)
+        _check_out(pred, "out[3] (pred)", (B, H, Lq), torch.float32, dev)
+        _check_out(actual, "out[4] (actual)", (B, H, Lq), torch.float32, dev)
     pw = aw = None
     if weighted_out:
         pw = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
         aw = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
-    faults = [] if fault is None else ([fault] if isinstance(fault, Fault) else list(fault))
-    arr = (FabftFault * max(1, len(faults)))(*[f.to_c() for f in faults])
+    arr, n = _faults_array(fault)
     _stream(dev)
     _check(_load().fabft_attn_fwd_inject_n(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                                         resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
-                                        int(bool(causal)), scale, arr, len(faults),
+                                        int(bool(causal)), scale, arr, n,
                                         pred.data_ptr(), actual.data_ptr(),
                                         pw.data_ptr() if pw is not None else None,
                                         aw.data_ptr() if aw is not None else None),
@@ -388,7 +485,7 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
     return o, resid, flags, pred, actual
 
 
-__all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_splitkv", "splitkv_workspace_bytes",
+__all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_debug", "attn_fwd_splitkv", "splitkv_workspace_bytes",
            "splitkv_default_splits",
            "global_check", "recompute_flagged", "Fault", "FabftError", "set_threshold",
            "set_score_check", "score_check_workspace_bytes", "get_score_threshold",

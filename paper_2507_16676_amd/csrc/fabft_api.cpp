@@ -86,6 +86,7 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.actual = nullptr;
   p.pred_w = nullptr;
   p.actual_w = nullptr;
+  p.s_lhs = p.s_rhs = p.s_bound = nullptr;
   p.wcheck = g_wcheck;
   p.nsplit = 1;
   p.split_tiles = 0;
@@ -247,10 +248,10 @@ int check_fault(const fabft_fault* f, int B, int H, int Lq, int Lk, int d, int c
 
 extern "C" {
 
-int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o, float* resid,
-                            uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
-                            float scale, const fabft_fault* faults, int nfaults, float* pred,
-                            float* actual, float* pred_w, float* actual_w) {
+int fabft_attn_fwd_debug(const void* q, const void* k, const void* v, void* o, float* resid,
+                         uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                         float scale, const fabft_fault* faults, int nfaults,
+                         const fabft_debug_out* out) {
   int n_qt = 0, grid = 0;
   int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
   if (rc != FABFT_OK) return rc;
@@ -258,10 +259,15 @@ int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o
   if (nfaults < 0 || nfaults > FABFT_MAX_FAULTS) return FABFT_E_FAULT;
   if (nfaults > 0 && !faults) return FABFT_E_NULL;
   fabft::FwdParams p = make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid);
-  p.pred = pred;
-  p.actual = actual;
-  p.pred_w = pred_w;
-  p.actual_w = actual_w;
+  if (out) {
+    p.pred = out->pred;
+    p.actual = out->actual;
+    p.pred_w = out->pred_w;
+    p.actual_w = out->actual_w;
+    p.s_lhs = out->score_lhs;
+    p.s_rhs = out->score_rhs;
+    p.s_bound = out->score_bound;
+  }
   for (int i = 0; i < nfaults; ++i) {
     const fabft_fault* f = faults + i;
     if (f->site == FABFT_SITE_NONE) continue;
@@ -270,6 +276,15 @@ int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o
     p.f[p.nf++] = fabft::FaultDesc{f->site, f->b * H + f->h, f->row, f->col, f->tile, f->bit};
   }
   return launch(p, d, causal, 2, B * H);
+}
+
+int fabft_attn_fwd_inject_n(const void* q, const void* k, const void* v, void* o, float* resid,
+                            uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                            float scale, const fabft_fault* faults, int nfaults, float* pred,
+                            float* actual, float* pred_w, float* actual_w) {
+  const fabft_debug_out out = {pred, actual, pred_w, actual_w, nullptr, nullptr, nullptr};
+  return fabft_attn_fwd_debug(q, k, v, o, resid, flags, B, H, Lq, Lk, d, causal, scale, faults,
+                              nfaults, &out);
 }
 
 int fabft_attn_fwd_inject(const void* q, const void* k, const void* v, void* o, float* resid,

@@ -29,6 +29,12 @@ struct FwdParams {
   float* actual;  // injection/debug kernels only; may be null
   float* pred_w;    // weighted check, debug kernels only; may be null
   float* actual_w;  // weighted check, debug kernels only; may be null
+  // score check, debug kernels only; may be null: the row's sum of raw
+  // scores over the key tiles without a mask (lhs), q_i . sum_k K_k over the
+  // same keys (rhs) and |q_i| . sum_k |K_k| (the bound); 0 with the check off
+  float* s_lhs;
+  float* s_rhs;
+  float* s_bound;
   int wcheck;     // 1: also run the weighted (alternating-sign) checksum
   // split over the keys (mode 3): workgroup (head, query tile, split) runs
   // key tiles [split*split_tiles, (split+1)*split_tiles) and writes the

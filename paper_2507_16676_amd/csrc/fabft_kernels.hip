@@ -855,6 +855,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     // weighted check: pred_w = c_w / l against sum_j (-1)^j O_ij (the same
     // threshold rule; |w_j| = 1 keeps M)
     float pred_w = 0.f;
+    float sc_lhs = 0.f, sc_rhs = 0.f, sc_bound = 0.f;   // score check (debug outputs)
     if constexpr (WCHK) {
       act_w = sum_xor32(act_w);
       pred_w = sum_xor32(aux[4] + aux[5]) * inv;
@@ -899,6 +900,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
       const float rs = lhs - rhs;
       nonfinite = nonfinite || nonfinite_bits(rs);
       if (!(__builtin_fabsf(rs) <= p.tau_s * ms + p.tau_abs)) f |= 8;
+      sc_lhs = lhs;
+      sc_rhs = rhs;
+      sc_bound = ms;
     }
     if (nonfinite) f |= 3;
     if (grp == 0 && qrow < Lq) {
@@ -910,6 +914,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
         if (p.actual) p.actual[ri] = act;
         if (p.pred_w) p.pred_w[ri] = pred_w;
         if (p.actual_w) p.actual_w[ri] = WCHK ? act_w : 0.f;
+        if (p.s_lhs) p.s_lhs[ri] = sc_lhs;
+        if (p.s_rhs) p.s_rhs[ri] = sc_rhs;
+        if (p.s_bound) p.s_bound[ri] = sc_bound;
       }
     }
   }

@@ -252,3 +252,29 @@ def test_score_check_workspace_and_switch():
         assert L.fabft_get_score_threshold() == pytest.approx(1e-3)
     finally:
         assert L.fabft_set_score_check(None, 0, 0.0) == F.FABFT_OK
+
+
+def test_caller_tensor_checks():
+    """Every caller-supplied tensor is checked before its pointer reaches the
+    library: shape, dtype, contiguity and device (here on CPU tensors; the
+    GPU tests run the same checks through the entry points)."""
+    import torch
+    cpu = torch.device("cpu")
+    t = torch.empty((2, 3, 5), dtype=torch.float32)
+    assert F._check_out(t, "t", (2, 3, 5), torch.float32, cpu) is t
+    with pytest.raises(ValueError, match="shape"):
+        F._check_out(t, "t", (2, 3, 6), torch.float32, cpu)
+    with pytest.raises(ValueError, match="float32"):
+        F._check_out(t.to(torch.float16), "t", (2, 3, 5), torch.float32, cpu)
+    with pytest.raises(ValueError, match="contiguous"):
+        F._check_out(torch.empty((2, 5, 3)).transpose(1, 2), "t", (2, 3, 5), torch.float32, cpu)
+    with pytest.raises(ValueError, match="on"):
+        F._check_out(t, "t", (2, 3, 5), torch.float32, torch.device("meta"))
+    with pytest.raises(ValueError, match="tensor"):
+        F._check_out(None, "t", (2, 3, 5), torch.float32, cpu)
+    ws = torch.empty(100, dtype=torch.float32)
+    assert F._check_workspace(ws, "ws", 400, cpu) is ws
+    with pytest.raises(ValueError, match="needed"):
+        F._check_workspace(ws, "ws", 401, cpu)
+    with pytest.raises(ValueError, match="contiguous"):
+        F._check_workspace(torch.empty((10, 20))[:, ::2], "ws", 4, cpu)

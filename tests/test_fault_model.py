@@ -402,3 +402,38 @@ def test_a_planted_sign_error_is_caught():
     dO_b = np.array(faulty[9][0]) - np.array(clean[9][0])
     assert np.allclose(dO_b, r["dO"], rtol=2 ** -7, atol=1e-9)
     assert not np.allclose(dO_b, -r["dO"], rtol=2 ** -7, atol=1e-9)
+
+
+@pytest.mark.parametrize("site,bit", [("S", 24), ("S", 29), ("S", 31), ("Q", 9), ("Q", 13), ("Q", 15)])
+def test_score_check_fault_brute_force(site, bit):
+    """The score check after an S or Q flip, by brute force: lhs sums the
+    scores as computed with the flipped value, rhs and the bound use the
+    final q (64-key tiles, causal 150 x 200)."""
+    Lq, Lk = 150, 200
+    q, k, _ = _inputs(Lq, Lk, 3, seed=77)
+    for i in (40, 100, 149):
+        r0 = FM.score_check_row(q, k, i, Lq, True)
+        n = r0["n"]
+        col = 3 if site == "S" else 1
+        tile = 0 if site == "S" else 1
+        f = FM.FaultSpec(site, i, col, tile, bit)
+        pr = FM.score_check_fault(q, k, i, Lq, True, f)
+        qi = [float(x) for x in q[i]]
+        lhs = 0.0
+        for kk in range(n):
+            if site == "Q" and kk == 64 * tile:
+                qi[col] = bf16_flip(qi[col], bit)
+            sc = sum(qi[j] * float(k[kk][j]) for j in range(3))
+            if site == "S" and kk == col:
+                sc = f32_flip(f32(sc), bit)
+            lhs += sc
+        if site == "Q" and n <= 64 * tile:
+            qi[col] = bf16_flip(qi[col], bit)
+        rhs = sum(qi[j] * sum(float(k[kk][j]) for kk in range(n)) for j in range(3))
+        ms = sum(abs(qi[j]) * sum(abs(float(k[kk][j])) for kk in range(n)) for j in range(3))
+        assert math.isclose(pr["lhs"], lhs, rel_tol=1e-12, abs_tol=1e-9 * (ms + 1))
+        assert math.isclose(pr["rhs"], rhs, rel_tol=1e-12, abs_tol=1e-9 * (ms + 1))
+        assert math.isclose(pr["ms"], ms, rel_tol=1e-12)
+        assert pr["nonfinite"] == (not math.isfinite(lhs - rhs) or not math.isfinite(ms))
+        if not pr["nonfinite"]:
+            assert pr["flag"] == (abs(lhs - rhs) > 2.0 ** -22 * ms)
