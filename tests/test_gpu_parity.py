@@ -61,12 +61,45 @@ def test_dec_l4096_rows():
 
 
 def test_long_l32768_rows():
+    """The 32768-token workload with 1% of each head's keys scaled by 8:
+    per head, 256 seeded rows of its own, rows 0 and Lq - 1, and the rows at
+    and just after 8 of that head's own x8 keys (drawn per head), where a
+    peaked score arrives late in the row and the checksum must be rescaled
+    with the output."""
+    import oracle
     w = W.WORKLOADS["long_l32768"]
-    inp_rows = W.make_inputs(w).peaked_rows[0, 0]
-    # rows at and just after a x8 key of head 0 (causal: they see it)
-    extra = tuple(int(r) for r in np.sort(inp_rows)[:8]) + tuple(int(r) + 1 for r in np.sort(inp_rows)[:8])
-    rows = W.sample_rows(w.Lq, 64, 0, must=(0, 1, w.Lq - 1) + extra)
-    _parity(w, rows=rows)
+    print(f"[parity] {w.name} B{w.B} H{w.H} Lq{w.Lq} Lk{w.Lk} d{w.d} causal={w.causal}",
+          flush=True)
+    inp = W.make_inputs(w)
+    q, k, v = G.dev_inputs(inp)
+    o, resid, flags, pred, actual = _run_all(q, k, v, w.causal, w.scale)
+    assert int((flags != 0).sum()) == 0
+    O = G.from_dev_bf16(o)
+    P = pred.double().cpu().numpy()
+    qf, kf, vf = inp.as_f32()
+    worst = {"o_max_abs": 0.0, "pred_max_abs": 0.0}
+    n_rows = 0
+    for b in range(w.B):
+        for h in range(w.H):
+            rng = np.random.default_rng(1000 + 97 * b + h)
+            peaked = inp.peaked_rows[b, h]
+            pick = rng.choice(peaked, size=8, replace=False)
+            must = (0, w.Lq - 1) + tuple(int(r) for r in pick) + tuple(int(r) + 1 for r in pick)
+            rows = W.sample_rows(w.Lq, 256, seed=1 + 97 * b + h, must=must)
+            assert len(rows) >= 256 + 2
+            ref = oracle.attention_head(qf[b, h], kf[b, h], vf[b, h], w.causal, w.scale,
+                                        rows=rows)
+            err = np.abs(O[b, h, rows] - ref["O"])
+            rel = err.sum() / np.abs(ref["O"]).sum()
+            perr = np.abs(P[b, h, rows] - ref["pred"])
+            prel = perr.sum() / np.abs(ref["pred"]).sum()
+            assert np.all(np.isfinite(O[b, h, rows]))
+            assert err.max() <= G.O_MAX_ABS and rel <= G.O_REL_L1, (b, h, err.max(), rel)
+            assert perr.max() <= G.O_MAX_ABS * np.sqrt(w.d) and prel <= G.O_REL_L1, (b, h)
+            worst["o_max_abs"] = max(worst["o_max_abs"], float(err.max()))
+            worst["pred_max_abs"] = max(worst["pred_max_abs"], float(perr.max()))
+            n_rows += len(rows)
+    print(f"[parity] {w.name}: {n_rows} rows over {w.B * w.H} heads, worst {worst}", flush=True)
 
 
 @pytest.mark.parametrize("d", [64, 96, 128, 256])
