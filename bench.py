@@ -30,6 +30,12 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_{workload}.json")
 KERNEL_SRC = os.path.join(ROOT, "paper_2507_16676_amd", "csrc", "fabft_kernels.hip")
 
 
+def w_bytes(w):
+    """Algorithmic bytes of one forward: Q, K, V read once (bf16), O written
+    once (bf16), resid (fp32) and flags (u8) per query row."""
+    return 2 * w.B * w.H * (2 * w.Lq * w.d + 2 * w.Lk * w.d) + 5 * w.B * w.H * w.Lq
+
+
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
@@ -41,7 +47,8 @@ def kernel_src_sha() -> str:
 
 def make_device_inputs(w, device):
     """Seeded N(0,1) inputs of the workload's shape and recipe, drawn on the
-    GPU (the timed path needs no host copy); bf16 round-to-nearest-even."""
+    GPU (no host copy; for the decode sweep, whose shapes have no oracle
+    leg); bf16 round-to-nearest-even."""
     import torch
     g = torch.Generator(device=device)
     g.manual_seed(w.seed)
@@ -63,6 +70,87 @@ def make_device_inputs(w, device):
                 k[b, h, idx] *= w.peaked_mult
     return (q.to(torch.bfloat16).contiguous(), k.to(torch.bfloat16).contiguous(),
             v.to(torch.bfloat16).contiguous())
+
+
+def host_inputs(w, device):
+    """The workload's seeded host recipe (workloads.make_inputs: numpy PCG64,
+    bf16), moved to the GPU; the oracle's baseline leg times heads of these
+    same tensors. Returns the host Inputs and the device tensors."""
+    import numpy as np
+    import torch
+    import workloads as W
+    inp = W.make_inputs(w)
+
+    def dev(bits):
+        t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+        return t.view(torch.bfloat16).to(device).contiguous()
+
+    return inp, (dev(inp.q), dev(inp.k), dev(inp.v))
+
+
+class SclkSampler:
+    """Samples the GPU's current shader clock (the starred line of
+    pp_dpm_sclk in sysfs) every `period` seconds on a host thread while
+    active; reports the median, min and max of the samples taken."""
+
+    def __init__(self, period: float = 0.002):
+        import glob
+        import threading
+        self.period = period
+        self.paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.samples = []
+        self._on = threading.Event()
+        self._stop = threading.Event()
+        self._thr = None
+        if self.paths:
+            self._thr = threading.Thread(target=self._run, daemon=True)
+            self._thr.start()
+
+    def _read(self):
+        import re
+        try:
+            with open(self.paths[0]) as f:
+                for line in f:
+                    if "*" in line:
+                        m = re.search(r"(\d+)\s*Mhz", line, re.I)
+                        return int(m.group(1)) if m else None
+        except OSError:
+            return None
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            if self._on.is_set():
+                v = self._read()
+                if v is not None:
+                    self.samples.append(v)
+            time.sleep(self.period)
+
+    def start(self):
+        self._on.set()
+
+    def pause(self):
+        self._on.clear()
+
+    def close(self):
+        self._stop.set()
+        if self._thr:
+            self._thr.join(timeout=1)
+
+    def summary(self):
+        if not self.samples:
+            return {"source": "pp_dpm_sclk" if self.paths else None, "samples": 0}
+        x = sorted(self.samples)
+        return {"source": "pp_dpm_sclk (sysfs, current level)", "samples": len(x),
+                "median_mhz": x[len(x) // 2], "min_mhz": x[0], "max_mhz": x[-1]}
+
+
+def percentile(xs, p):
+    x = sorted(xs)
+    if not x:
+        return None
+    i = min(len(x) - 1, max(0, int(round(p / 100.0 * (len(x) - 1)))))
+    return x[i]
 
 
 def time_launches(fn, steps, stream):
@@ -134,10 +222,20 @@ def copy_probe(mib: int, dev):
     log(f"[bench] copy probe: {mib} MiB device-to-device")
 
 
-def cpu_baseline(w, target_s: float):
-    """Time the fp64 oracle on the host for a bounded sample of the workload:
-    whole heads (all query rows) of batch entry 0, drawn with the same
-    recipe, as many as fit in about `target_s` seconds."""
+def blas_info():
+    """Name and version of numpy's BLAS (numpy.show_config)."""
+    import numpy as np
+    try:
+        d = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        return f"{d.get('name')} {d.get('version')}"
+    except Exception:   # older numpy: no dict mode
+        return "numpy BLAS (vendor not reported)"
+
+
+def cpu_baseline(w, inp, target_s: float):
+    """Time the fp64 oracle on the host on heads of the same seeded tensors
+    the GPU ran (workloads.make_inputs), whole heads in (b, h) order, all
+    query rows, as many as fit in about `target_s` seconds."""
     import numpy as np
     import oracle
     import workloads as W
@@ -147,24 +245,44 @@ def cpu_baseline(w, target_s: float):
                        if i.get("user_api") == "blas"), default=1)
     except Exception:   # threadpoolctl missing: report the affinity mask
         threads = len(os.sched_getaffinity(0))
-    one = w.with_(B=1, H=1)
-    inp = W.make_inputs(one)
-    q, k, v = inp.as_f32()
+    heads = [(b, h) for b in range(w.B) for h in range(w.H)]
+
+    def run(sel):
+        for (b, h) in sel:
+            qf, kf, vf = (W.bf16_bits_to_f32(x[b, h]) for x in (inp.q, inp.k, inp.v))
+            oracle.attention(qf[None, None], kf[None, None], vf[None, None], w.causal, w.scale)
+
     t0 = time.perf_counter()
-    oracle.attention(q, k, v, w.causal, w.scale)
+    run(heads[:1])
     t_head = time.perf_counter() - t0
-    n_heads = int(max(1, min(w.B * w.H, math.floor(target_s / max(t_head, 1e-6)))))
-    sample = w.with_(B=1, H=n_heads)
-    inp = W.make_inputs(sample)
-    q, k, v = inp.as_f32()
+    n_heads = int(max(1, min(len(heads), math.floor(target_s / max(t_head, 1e-6)))))
     t0 = time.perf_counter()
-    oracle.attention(q, k, v, w.causal, w.scale)
+    run(heads[:n_heads])
     dt = time.perf_counter() - t0
-    tflops = sample.flops / dt / 1e12
-    return {"value": tflops, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"{n_heads} of {w.B * w.H} heads (b=0, all {w.Lq} rows), "
-                      f"{dt:.2f} s, fp64 numpy",
-            "seconds": dt, "blas": "numpy BLAS"}
+    flops = w.flops * n_heads / len(heads)
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"the first {n_heads} of the {len(heads)} heads of the same seeded tensors "
+                      f"(b, h order, all {w.Lq} query rows each), {dt:.2f} s, fp64 numpy; "
+                      f"the value is their attention flops (4 d per visible pair) over that time",
+            "seconds": dt, "heads": n_heads, "blas": blas_info(),
+            "blas_threads": int(threads), "affinity_cores": len(os.sched_getaffinity(0))}
+
+
+def time_flushed(fn, steps, stream, flush):
+    """Per-launch time (ms) of `steps` calls with `flush` (a write that
+    evicts the caches) before each, timed with events around the call only."""
+    import torch
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        flush()
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in evs]
 
 
 def main():
@@ -188,6 +306,12 @@ def main():
     ap.add_argument("--score-check", action="store_true",
                     help="also run the score check (an extension; its K-sum pre-pass is timed)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--ramp-ms", type=float, default=300.0,
+                    help="untimed launches for at least this long before the timed block "
+                         "(clock ramp), whatever --warmup says")
+    ap.add_argument("--flush-mib", type=int, default=0,
+                    help="also time the launches with a write of this many MiB before each "
+                         "(cold caches; 512 exceeds the 256 MB Infinity Cache)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="also run one plain device copy of this size (calibrates "
                          "the FETCH_SIZE / WRITE_SIZE counters)")
@@ -218,7 +342,7 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     log(f"[bench] workload {w.name}: B{w.B} H{w.H} Lq{w.Lq} Lk{w.Lk} d{w.d} causal={w.causal}")
-    q, k, v = make_device_inputs(w, dev)
+    inp, (q, k, v) = host_inputs(w, dev)
     if args.score_check:
         sws = torch.empty(F.score_check_workspace_bytes(w.B, w.H, w.Lk, w.d), dtype=torch.uint8,
                           device=dev)
@@ -235,34 +359,52 @@ def main():
         F.attn_fwd(q, k, v, causal=w.causal, scale=w.scale, check=False, out=(o,))
 
     # fault-free check first: counting the flags waits on the host, and the
-    # GPU lowers its clock while idle (the first ~25 launches after such a
-    # gap run ~15% slower), so the warmup runs last, right before the timing
+    # GPU lowers its clock while idle, so the warmup runs last, right before
+    # the timing
     on()
     torch.cuda.synchronize()
     nflag = int((flags != 0).sum())
     for _ in range(args.warmup):
         on()
         off()
-    torch.cuda.synchronize()
-    log(f"[bench] warmup done; fault-free flagged rows: {nflag}")
+    # clock ramp: keep launching for at least --ramp-ms of wall time whatever
+    # --warmup says (the shader clock rises only under sustained load; the
+    # first launches after an idle gap run up to ~15% slow)
+    t0 = time.perf_counter()
+    n_ramp = 0
+    while True:
+        for _ in range(10):
+            on()
+        n_ramp += 10
+        torch.cuda.synchronize()
+        if (time.perf_counter() - t0) * 1e3 >= args.ramp_ms:
+            break
+    ramp_ms = (time.perf_counter() - t0) * 1e3
+    log(f"[bench] warmup done ({args.warmup} on/off pairs, then {n_ramp} launches over "
+        f"{ramp_ms:.0f} ms); fault-free flagged rows: {nflag}")
 
+    sclk = SclkSampler()
+    sclk.start()
     # ---- timed region: exactly `steps` checksum-on steps
     total_ms, per = time_launches(on, args.steps, stream)
     ms = total_ms / args.steps
     flops = w.flops
     tflops = flops / (ms * 1e-3) / 1e12
     avg_launch_ms = sum(per) / len(per)
-    log(f"[bench] checksum on: {ms:.4f} ms/step, {tflops:.1f} TFLOP/s")
+    log(f"[bench] checksum on: {ms:.4f} ms/step, {tflops:.1f} TFLOP/s "
+        f"(per launch p10 {percentile(per, 10):.4f}, p90 {percentile(per, 90):.4f} ms)")
 
     # ---- checksum off, and interleaved on/off rounds for the overhead
-    ratios, on_ms, off_ms = [], [], []
+    ratios, on_ms, off_ms, off_per = [], [], [], []
     k_round = max(3, args.steps // 2)
     for r in range(args.rounds):
         t_on, _ = time_launches(on, k_round, stream)
-        t_off, _ = time_launches(off, k_round, stream)
+        t_off, per_off = time_launches(off, k_round, stream)
         on_ms.append(t_on / k_round)
         off_ms.append(t_off / k_round)
+        off_per += per_off
         ratios.append(t_on / t_off)
+    sclk.pause()
     ratios.sort()
     overhead = 100.0 * (ratios[len(ratios) // 2] - 1.0)
     ms_off = sorted(off_ms)[len(off_ms) // 2]
@@ -270,6 +412,27 @@ def main():
     tflops_off = flops / (ms_off * 1e-3) / 1e12
     log(f"[bench] checksum off: {ms_off:.4f} ms/step, {tflops_off:.1f} TFLOP/s; "
         f"interleaved on {ms_on_r:.4f} ms/step; overhead {overhead:.2f}%")
+    sclk.close()
+    clk = sclk.summary()
+    if clk.get("samples"):
+        log(f"[bench] shader clock during the timed launches: median {clk['median_mhz']} MHz "
+            f"({clk['min_mhz']}-{clk['max_mhz']}, {clk['samples']} samples)")
+
+    # ---- the same launches with the caches flushed before each (a write
+    # larger than the 256 MB Infinity Cache), timed around the call only
+    cold = None
+    if args.flush_mib > 0:
+        buf = torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
+        per_cold = time_flushed(on, args.steps, stream, lambda: buf.fill_(1))
+        per_cold_off = time_flushed(off, args.steps, stream, lambda: buf.fill_(1))
+        c_on = sorted(per_cold)[len(per_cold) // 2]
+        c_off = sorted(per_cold_off)[len(per_cold_off) // 2]
+        cold = {"flush_mib": args.flush_mib, "ms_per_launch_median": round(c_on, 5),
+                "tflops": round(flops / (c_on * 1e-3) / 1e12, 2),
+                "checksum_off_ms_median": round(c_off, 5),
+                "overhead_pct": round(100.0 * (c_on / c_off - 1.0), 3)}
+        log(f"[bench] cold cache: on {c_on:.4f} ms, off {c_off:.4f} ms per launch")
+        del buf
 
     # ---- roofline of the dominant kernel (the checksum-on forward; one
     # launch per step)
@@ -295,9 +458,9 @@ def main():
     cpu = None
     if not args.no_cpu_baseline:
         log("[bench] timing the fp64 oracle on the host ...")
-        cpu = cpu_baseline(w, args.cpu_seconds)
+        cpu = cpu_baseline(w, inp, args.cpu_seconds)
         log(f"[bench] oracle: {cpu['value'] * 1e3:.2f} GFLOP/s on {cpu['cores']} threads "
-            f"({cpu['sample']})")
+            f"({cpu['sample']}; {cpu['blas']})")
 
     line = {
         "metric": "attention TFLOP/s (bf16, 1 GPU) + % MFMA peak; checksum overhead %; "
@@ -305,7 +468,7 @@ def main():
         "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded N(0,1), drawn on the GPU)",
+        "dtype": "bf16", "data": "synthetic (seeded N(0,1), numpy PCG64 host recipe, bf16)",
         "config": {"workload": w.name, "B": w.B, "H": w.H, "Lq": w.Lq, "Lk": w.Lk,
                    "d": w.d, "causal": w.causal, "scale": w.scale,
                    "checksum": "on" + ("+weighted" if args.weighted else "")
@@ -314,6 +477,18 @@ def main():
         "checksum_off": {"ms_per_step": round(ms_off, 5), "tflops": round(tflops_off, 2)},
         "checksum_overhead_pct": round(overhead, 3),
         "fault_free_flagged_rows": nflag,
+        "per_launch_ms": {"p10": round(percentile(per, 10), 5),
+                          "median": round(percentile(per, 50), 5),
+                          "p90": round(percentile(per, 90), 5)},
+        "checksum_off_per_launch_ms": {"p10": round(percentile(off_per, 10), 5),
+                                       "median": round(percentile(off_per, 50), 5),
+                                       "p90": round(percentile(off_per, 90), 5)},
+        "interleaved_on_ms_per_step": round(ms_on_r, 5),
+        "clock_ramp_ms": round(ramp_ms, 1),
+        "sclk": clk,
+        "cache": (f"hot: launches back to back (working set {w_bytes(w) / 1e6:.0f} MB against "
+                  f"the 256 MB Infinity Cache)"),
+        "cold_cache": cold,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

@@ -31,11 +31,24 @@ def test_flop_count(name, flops):
 
 
 def test_cpu_baseline_record():
+    """The oracle leg times whole heads of the bench's own seeded tensors and
+    names the BLAS it ran on."""
     w = W.WORKLOADS["bert_l128"]
-    rec = bench.cpu_baseline(w, target_s=0.2)
+    inp = W.make_inputs(w)
+    rec = bench.cpu_baseline(w, inp, target_s=0.2)
     assert rec["kind"] == "oracle" and rec["unit"] == "TFLOP/s"
-    assert rec["value"] > 0 and rec["cores"] >= 1
-    assert "heads" in rec["sample"] and rec["seconds"] > 0
+    assert rec["value"] > 0 and rec["cores"] >= 1 and rec["affinity_cores"] >= 1
+    assert "heads of the same seeded tensors" in rec["sample"] and rec["seconds"] > 0
+    assert 1 <= rec["heads"] <= w.B * w.H
+    assert rec["blas"] and "not reported" not in rec["blas"]
+
+
+def test_percentile_and_bytes():
+    assert bench.percentile([5, 1, 4, 2, 3], 50) == 3
+    assert bench.percentile([5, 1, 4, 2, 3], 10) == 1 and bench.percentile([1, 2, 3], 90) == 3
+    w = W.WORKLOADS["dec_l4096"]
+    # Q, K, V read and O written once in bf16, 5 bytes of resid and flags per row
+    assert bench.w_bytes(w) == 4 * 32 * (4 * 4096 * 128 * 2) + 5 * 4 * 32 * 4096
 
 
 def test_kernel_hash_is_the_source_hash():
