@@ -99,8 +99,9 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v,
 
 /*
  * Bytes of workspace that fabft_attn_fwd_splitkv needs: one partial-state
- * record of (d + 4) floats per (b, h, query row, split). Negative status for
- * d not 64/128, a size < 1 or nsplit outside 1..64.
+ * record of (w + 4) floats per (b, h, query row, split), w the compute width
+ * (d, or 128 for d = 96). Negative status for d not 64, 96, 128 or 256, a size
+ * < 1 or nsplit outside 1..64.
  */
 long long fabft_splitkv_workspace_bytes(int B, int H, int Lq, int d, int nsplit);
 
@@ -262,8 +263,14 @@ enum {
      positives): */
   FABFT_SITE_C = 5,    /* fp32 checksum accumulator pair c = c_hi + c_lo of
                           query row `row` (col 0: c_hi, col 1: c_lo) after
-                          the update of key tile `tile` */
-  FABFT_SITE_L = 6,    /* fp32 accumulator l of the row after key tile `tile` */
+                          the update of key tile `tile`. c and l of a row
+                          are held as two partial sums, one per half of the
+                          keys (keys k with k mod 16 < 8, and the others),
+                          added at the end; this site flips the first half's
+                          register */
+  FABFT_SITE_L = 6,    /* fp32 accumulator l of the row after key tile
+                          `tile` (the first key half's partial sum, as for
+                          FABFT_SITE_C) */
   FABFT_SITE_M = 7,    /* fp32 running max (scale * log2 e units) of the row,
                           as held by the lane of the row's first key half,
                           after the exponentials of key tile `tile` */

@@ -24,12 +24,13 @@ f = x'/x gives:
        dO_ij = (f - 1) sum_{k <= end of tile t} P_ik V_kj,  dpred_i = 0
   V  (V_kj in one workgroup's copy, after its sumrow was taken; V' = V + dV):
        dO_ij = P_ik dV for every row i of that workgroup that sees key k
-  C  (one part of the checksum accumulator c_i = c_hi + c_lo after tile t):
-       dO = 0,  dpred_i = (f - 1) sum_{k <= end of tile t} P_ik part_k
+  C  (one part of the checksum accumulator c_i = c_hi + c_lo after tile t,
+     as held for the row's first key half):
+       dO = 0,  dpred_i = (f - 1) sum_{k <= end of tile t, k in H} P_ik part_k
   VS (one part of the sumrow record of key k in one workgroup):
        dO = 0,  dpred_i = P_ik (part'_k - part_k) for its rows that see k
-  L  (the accumulator l_i after tile t): O and pred are both divided by
-       1 + (f - 1) F_t with F_t = sum_{k <= end of tile t} P_ik
+  L  (the accumulator l_i after tile t, first key half): O and pred are both
+       divided by 1 + (f - 1) F_t with F_t = sum_{k <= end of tile t, k in H} P_ik
   S  (the raw score q_i . k_k), Q (q_ij from key tile t on): the scores
        change upstream of the checksum tap; O follows the plain definition
        with the changed scores and pred moves with it (resid stays 0).
@@ -47,6 +48,9 @@ the library's header gives for each site):
     alike with 1 and the sumrow parts;
   * the sumrow record of key k is vs_k in fp32 split into bf16 hi = bf16(vs)
     and lo = bf16(vs - hi);
+  * c and l of a row are held as two partial sums, one per key half: H, the
+    keys k with k mod 16 < 8, and the rest (one register each, added at the
+    end); the C and L sites flip the register of H;
   * a wave of 32 query rows computes every key tile up to the diagonal of
     its last row (causal), so a non-finite V_kj or sumrow part also reaches
     the rows of that wave that give key k the weight 0 (0 * inf is NaN).
@@ -180,7 +184,14 @@ def row_frame(s: np.ndarray, vis: np.ndarray, sl2: float, v: np.ndarray,
     l = np.zeros(nt)
     chi = np.zeros(nt)
     clo = np.zeros(nt)
+    # the same sums over the first key half (keys k with k mod 16 < 8), the
+    # part one lane of the row holds
+    h0 = (np.arange(Lk) % 16) < 8
+    l0 = np.zeros(nt)
+    chi0 = np.zeros(nt)
+    clo0 = np.zeros(nt)
     run_o, run_l, run_hi, run_lo = np.zeros(d), 0.0, 0.0, 0.0
+    run_l0, run_hi0, run_lo0 = 0.0, 0.0, 0.0
     for t in range(nt):
         a, b = t * key_tile, min(Lk, (t + 1) * key_tile)
         vt = vis[a:b]
@@ -191,6 +202,7 @@ def row_frame(s: np.ndarray, vis: np.ndarray, sl2: float, v: np.ndarray,
             alpha = 2.0 ** (ref - new)
             run_o, run_l = run_o * alpha, run_l * alpha
             run_hi, run_lo = run_hi * alpha, run_lo * alpha
+            run_l0, run_hi0, run_lo0 = run_l0 * alpha, run_hi0 * alpha, run_lo0 * alpha
         ref = new
         refs[t] = ref
         if vt.any():
@@ -201,8 +213,14 @@ def row_frame(s: np.ndarray, vis: np.ndarray, sl2: float, v: np.ndarray,
             run_l = run_l + w.sum()
             run_hi = run_hi + w @ hi[a:b]
             run_lo = run_lo + w @ lo[a:b]
+            w0 = np.where(h0[a:b], w, 0.0)
+            run_l0 = run_l0 + w0.sum()
+            run_hi0 = run_hi0 + w0 @ hi[a:b]
+            run_lo0 = run_lo0 + w0 @ lo[a:b]
         o[t], l[t], chi[t], clo[t] = run_o, run_l, run_hi, run_lo
-    return {"ref": refs, "ptil": ptil, "o": o, "l": l, "c_hi": chi, "c_lo": clo}
+        l0[t], chi0[t], clo0[t] = run_l0, run_hi0, run_lo0
+    return {"ref": refs, "ptil": ptil, "o": o, "l": l, "c_hi": chi, "c_lo": clo,
+            "l_half": l0, "c_hi_half": chi0, "c_lo_half": clo0}
 
 
 def _sumrow_parts(v: np.ndarray):
@@ -279,6 +297,7 @@ def fault_effect(q, k, v, causal: bool, scale: float, fault: FaultSpec, key_tile
     sl2 = exp2_scale(scale)
     site = fault.site
     vs, hi, lo = _sumrow_parts(v)
+    half0 = (np.arange(Lk) % 16) < 8   # keys of the row's first key half
 
     def base(i):
         vis = _visible(i, Lq, Lk, causal)
@@ -333,8 +352,9 @@ def fault_effect(q, k, v, causal: bool, scale: float, fault: FaultSpec, key_tile
         elif site == "C":
             fr = row_frame(s, vis, sl2, v, hi, lo, key_tile)
             t = fault.tile
-            key = "c_hi" if fault.col == 0 else "c_lo"
-            parts = hi if fault.col == 0 else lo
+            key = "c_hi_half" if fault.col == 0 else "c_lo_half"
+            # the flipped register holds the first key half only
+            parts = np.where(half0, hi if fault.col == 0 else lo, 0.0)
             x = float(np.float32(fr[key][t]))
             xn = flip_f32(x, fault.bit)
             if not np.isfinite(xn):
@@ -354,12 +374,16 @@ def fault_effect(q, k, v, causal: bool, scale: float, fault: FaultSpec, key_tile
         elif site == "L":
             fr = row_frame(s, vis, sl2, v, hi, lo, key_tile)
             t = fault.tile
-            x = float(np.float32(fr["l"][t]))
+            x = float(np.float32(fr["l_half"][t]))
             xn = flip_f32(x, fault.bit)
             e = _tile_end(t, key_tile, Lk)
-            # l' / l = (weight after tile t) + f (weight up to it), summed
-            # apart so that nothing cancels when f is tiny
-            den = float(P[e:].sum()) + (xn / x) * float(P[:e].sum()) if np.isfinite(xn) else np.inf
+            # l' / l = (weight outside the flipped sum) + f (weight in it),
+            # summed apart so that nothing cancels when f is tiny
+            inside = np.zeros(Lk, dtype=bool)
+            inside[:e] = True
+            inside &= half0
+            den = (float(P[~inside].sum()) + (xn / x) * float(P[inside].sum())
+                   if np.isfinite(xn) else np.inf)
             if not (den > 0.0) or not np.isfinite(den):
                 # l' not positive or not finite: the kernel writes O = 0, pred = 0
                 # (the change is -O: the rounding of O's own weights bounds it)

@@ -17,10 +17,12 @@ kernel (which is bitwise deterministic):
   is bitwise unchanged (an alarm with a correct result, the paper's sense);
   Silent = not flagged and significant; Benign = none of these.
 
-The headline rate is Detected / (Detected + Silent) over exponent-bit flips
-(fp32 bits 23-30, bf16 bits 7-14) at the P, O and V sites; S-site flips
-happen before the checksum tap and change O and pred consistently, so they
-are reported separately.
+The rate reported is Detected / (Detected + Silent) over exponent-bit flips
+(fp32 bits 23-30, bf16 bits 7-14), over all sites the campaign draws (S, P,
+O, V: headline_with_S) and over P, O and V alone (headline): S-site flips
+happen before the checksum tap and change O and pred consistently, so the
+output checksum sees them only through non-finite values, and the optional
+score check is what covers them.
 
 Only the faulted head is recomputed per run (heads are independent, and the
 per-head computation does not depend on the others). Runs are drawn from
@@ -292,6 +294,16 @@ def summarize(path):
         hw = z * math.sqrt(p * (1 - p) / n + z * z / (4 * n * n)) / den
         return (max(0.0, c - hw), min(1.0, c + hw))
 
+    def exp_rate(sites):
+        c = {"detected": 0, "silent": 0}
+        for r in recs:
+            if r["site"] in sites and r["exponent_bit"] and r["outcome"] in c:
+                c[r["outcome"]] += 1
+        m = c["detected"] + c["silent"]
+        return {"detected": c["detected"], "silent": c["silent"],
+                "rate": c["detected"] / m if m else float("nan"),
+                "wilson95": wilson(c["detected"], m)}
+
     head = {"detected": 0, "silent": 0}
     for r in recs:
         if r["site"] in ("P", "O", "V") and r["exponent_bit"]:
@@ -338,6 +350,11 @@ def summarize(path):
             "headline": {"what": "exponent-bit flips at P, O, V: detected / (detected + silent)",
                          "detected": head["detected"], "silent": head["silent"],
                          "rate": rate, "wilson95": wilson(head["detected"], n)},
+            "headline_with_S": {"what": "exponent-bit flips at S, P, O, V (every site the "
+                                        "campaign draws): detected / (detected + silent)",
+                                **exp_rate(("S", "P", "O", "V"))},
+            "S_exponent": {"what": "exponent-bit flips at S alone (before the checksum tap)",
+                           **exp_rate(("S",))},
             "headline_global": {"what": "the same significant runs, flagged by the per-head "
                                         "global check (Alg. 3 single check)",
                                 "detected": gl["detected"], "silent": gl["silent"],

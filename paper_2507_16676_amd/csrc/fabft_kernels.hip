@@ -40,13 +40,18 @@
 //    of the workgroup, the paper's shared adder.
 //  * The weights p~ = bf16(p) feed the P V MFMA; l and the checksum c use
 //    exactly those p~, so that the rounding of P cancels between pred and
-//    actual. They come from one more 32x32x16 MFMA per 16-key step with the
-//    same P^T register as B operand and the 8-row sum operand as A:
-//    accumulator elements 0-2 of lanes 0-31 are c_hi, c_lo and l of their
-//    query, rescaled like o (Eq. 10 carries c as an extra row of V^T). Each
-//    output column is one query, so a non-finite p~ in one row cannot reach
-//    the sums of another (a 16x16x32 on the same register would mix the two
-//    16-query halves of the block).
+//    actual. They come from two 4x4x4 MFMAs (16 blocks) per 16-key step on
+//    the same P^T register as B operand: lane 4b+j is column j of block b
+//    with its own query, and lanes 4b..4b+3 supply the rows [sumrow hi;
+//    sumrow lo; ones; 0] of A, so element i of a lane accumulates c_hi,
+//    c_lo and l of its query over its half of the keys (4 registers;
+//    lanes l and l+32 add up at the end), rescaled like o (Eq. 10 carries c
+//    as an extra row of V^T). Each output column is one query, so a
+//    non-finite p~ in one row cannot reach the sums of another (a 16x16x32
+//    on the same register would mix the two 16-query halves of the block).
+//    With the weighted check two more 4x4x4 products per 8 keys carry the
+//    weighted sums (rows [weighted hi; weighted lo; 0; 0]) in 4 more
+//    registers; c and l come out the same either way.
 //  * Masking (causal diagonal tiles, the ragged last tile) sets a score to
 //    -inf, whose exponential is exactly 0.
 //  * Lazy rescaling: the running max used for the exponentials is moved only
@@ -102,6 +107,14 @@ constexpr uint32_t kAlt = 0xbf803f80u;   // bf16 pair (1.0, -1.0): weights (-1)^
 __device__ __forceinline__ f32x16 mfma32(u32x4 a, u32x4 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(
       __builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+}
+
+// 16 independent 4x4x4 bf16 products: block b = lane / 4 takes A row i from
+// lane 4b + i and B column j from lane 4b + j (4 k values each) and leaves
+// D[i][j] in element i of lane 4b + j (checked with a probe on gfx950)
+__device__ __forceinline__ f32x4 mfma4(u32x2 a, u32x2 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_4x4x4bf16_1k(__builtin_bit_cast(s16x4, a),
+                                               __builtin_bit_cast(s16x4, b), c, 0, 0, 0);
 }
 
 // a.lo*b.lo + a.hi*b.hi + c on packed bf16 pairs, fp32 accumulate
@@ -217,13 +230,13 @@ struct Tile {
 
 // Rows of the small A operand that yields c and l: sumrow(V) as bf16 hi and
 // lo parts, ones, zeros, and the weighted row sums sum_j (-1)^j V_kj as hi
-// and lo parts, padded to 8 rows (one wave-wide 16-byte load per 16 keys).
-// MFMA rows 0, 1, 2 read rows VsHi, VsLo, Ones; MFMA rows 8, 9 read WHi, WLo
-// (accumulator elements 4, 5 of lanes 0-31); the others read the zero row.
-// Below d = 256 a row holds the tile's 64 keys plus 8 unused ones: with
-// 144-byte rows, rows 0-3 start 36 banks apart and one read touches no bank
-// twice (128-byte rows put rows 0 and 2, and 1 and 3, on the same banks). At
-// d = 256 (one wave per SIMD, no register to spare) the rows stay 128 bytes.
+// and lo parts, padded to 8 rows. Lane 4b + i of a 4x4x4 product reads row i
+// (VsHi, VsLo, Ones, Zero), for the weighted sums WHi, WLo, Zero, Zero: one
+// wave-wide 16-byte load per 16 keys. Below d = 256 a row holds the tile's 64
+// keys plus 8 unused ones: with 144-byte rows, rows 0-3 start 36 banks apart
+// and one read touches no bank twice (128-byte rows put rows 0 and 2, and 1
+// and 3, on the same banks). At d = 256 (one wave per SIMD, LDS for two
+// 64 KiB stages) the rows stay 128 bytes.
 enum { kRowVsHi = 0, kRowVsLo = 1, kRowOnes = 2, kRowZero = 3, kRowWHi = 4, kRowWLo = 5,
        kVsmRows = 8 };
 
@@ -288,14 +301,18 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   } else if (CAUSAL) {
     const int BH = G / p.n_qt;
     if ((BH & 7) == 0) {
-      // XCD x owns heads x, x + 8, ...; it runs them kCausalBand heads at a
+      // XCD x owns heads x, x + 8, ...; it runs them a band of heads at a
       // time, each band longest tile first. The query tiles of a band stream
       // the same few K/V tiles at about the same time, so one HBM read
-      // serves several of them from L2.
+      // serves several of them from L2. A band holds as few heads as still
+      // give the XCD's 32 CUs at least 64 query tiles (at most kCausalBand):
+      // with long rows one head suffices, and all of an XCD's tiles then
+      // share one head's K/V.
+      const int bandw = min(kCausalBand, max(1, (64 + p.n_qt - 1) / p.n_qt));
       const int xcd = bid & 7, slot = bid >> 3;
-      const int band = slot / (kCausalBand * p.n_qt);
-      const int h0 = band * kCausalBand;
-      const int nb = min(kCausalBand, (BH >> 3) - h0);
+      const int band = slot / (bandw * p.n_qt);
+      const int h0 = band * bandw;
+      const int nb = min(bandw, (BH >> 3) - h0);
       const int w = slot - h0 * p.n_qt;
       const int qr = w / nb;
       bh = (h0 + w - qr * nb) * 8 + xcd;
@@ -351,7 +368,10 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   f32x16 oacc[NDB];
 #pragma unroll
   for (int b = 0; b < NDB; ++b) oacc[b] = f32x16{};
-  f32x16 aux = {};                    // lanes < 32: [0] c_hi, [1] c_lo, [2] l of query mrow
+  // c / l accumulator of this lane's query: [0] c_hi, [1] c_lo, [2] l over
+  // the lane's half of the keys (4x4x4 products; the two halves add up at
+  // the end); with the weighted check, auxw [0] c_w hi, [1] c_w lo alike
+  f32x4 aux = {}, auxw = {};
   float s_lhs = 0.f;                  // score check: sum of this lane's scores in full tiles
   float m2_run = -__builtin_inff();   // running max, exp2 domain (s * scale * log2 e)
   const float sl2 = p.sl2;
@@ -364,11 +384,13 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   }
   // row of the c / l operand that MFMA row mrow reads (rows 0, 1 only with
   // the checksum, rows 8, 9 only with the weighted one)
-  const int vsm_row = mrow == 2                ? (int)kRowOnes
-                      : (!CHECK)               ? (int)kRowZero
-                      : mrow < 2               ? mrow
-                      : (WCHK && (mrow == 8 || mrow == 9)) ? (int)kRowWHi + (mrow - 8)
-                                               : (int)kRowZero;
+  // 4x4x4 form: lane 4b + i supplies row i of block b's A: sumrow hi, lo,
+  // ones, zeros (the c rows read zeros without the checksum); for the
+  // weighted sums, weighted hi, lo, zeros, zeros
+  const int vsm_row4 = (lane & 3) == 2 ? (int)kRowOnes
+                       : (!CHECK || (lane & 3) == 3) ? (int)kRowZero
+                                                     : (lane & 3);
+  const int vsm_roww = (lane & 3) < 2 ? (int)kRowWHi + (lane & 3) : (int)kRowZero;
 
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
   // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk read as
@@ -408,24 +430,36 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     }
   };
 
-  // ---- sumrow(V) of the tile in stage S (Eq. 4): TPK threads per key
+  // ---- sumrow(V) of the tile in stage S (Eq. 4): TPK threads per key on
+  // the first SW waves. At D = 128 only waves 0-3 (one per SIMD) take it,
+  // four threads per key: every SIMD spends one wave's vector instructions
+  // on it rather than two (the sums are the same work either way; the
+  // per-key reduction and the hi / lo split are paid once per four lanes
+  // instead of eight).
   auto sumrow = [&](auto S_) __attribute__((always_inline)) {
     constexpr int S = decltype(S_)::value;
-    constexpr int TPK = kThreads / BC;   // threads per key
-    constexpr int CPT = CPR / TPK;       // 16-byte chunks per thread
-    static_assert(TPK * BC == kThreads && CPT * TPK == CPR, "sumrow covers the tile");
+    constexpr int SW = (D == 128) ? 4 : kWaves;   // waves taking part
+    constexpr int TPK = 64 * SW / BC;             // threads per key
+    constexpr int CPT = CPR / TPK;                // 16-byte chunks per thread
+    static_assert(TPK * BC == 64 * SW && CPT * TPK == CPR, "sumrow covers the tile");
+    if constexpr (SW < kWaves) {
+      if (wave >= SW) return;                     // wave-uniform
+    }
     const uint16_t* const sv = ring.v[S];
     uint16_t(*const svsm)[Ring<D>::VS] = ring.vsm[S];
     const int key = tid / TPK, part = tid % TPK;
     float a = 0.f, aw = 0.f;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
-      // at d = 128: chunk part + 8 j, j = i ^ (key mod 2), so that the two
-      // keys of one 16-lane read pass (keys 2m, 2m+1) take opposite halves
-      // of the row, whose banks the V swizzle keeps apart (reading chunks
-      // 2 part + i put both keys on the same banks); every key still reads
-      // all of its chunks. Other widths read CPT consecutive chunks.
-      const int c = CPT == 2 ? part + TPK * (i ^ (key & 1)) : CPT * part + i;
+      // at d = 128: chunk part + 4 i. A 16-lane read pass covers keys
+      // 4m .. 4m+3 (parts 0-3 each); the V swizzle stores logical chunk c of
+      // key r at c ^ 4(r mod 4), so the pass reads 16 distinct chunks of the
+      // 256-byte rows: no bank conflict. At d = 64: chunk part + 4 j,
+      // j = i ^ (key mod 2), so that the keys of one pass take opposite
+      // halves of the row, whose banks the V swizzle keeps apart. d = 256
+      // reads CPT consecutive chunks.
+      const int c = D == 128 ? part + TPK * i
+                  : CPT == 2 ? part + TPK * (i ^ (key & 1)) : CPT * part + i;
       const u32x4 ch = *reinterpret_cast<const u32x4*>(&sv[Tile<D>::vidx(key, c)]);
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -590,14 +624,28 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
 #pragma unroll
         for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) aux[i] *= alpha;
+      for (int i = 0; i < 4; ++i) aux[i] *= alpha;
+      if constexpr (WCHK) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) auxw[i] *= alpha;
+      }
     }
+    // each 8-key slice of p~ in two 4x4x4 products: the lane's own query
+    // is its column, so rows never mix (a non-finite p~ stays in its row)
 #pragma unroll
     for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(&svsm[vsm_row][32 * kb + 16 * h + 8 * grp]);
-        aux = mfma32(a, pb[kb][h], aux);
+        const u32x4 a =
+            *reinterpret_cast<const u32x4*>(&svsm[vsm_row4][32 * kb + 16 * h + 8 * grp]);
+        aux = mfma4(u32x2{a[0], a[1]}, u32x2{pb[kb][h][0], pb[kb][h][1]}, aux);
+        aux = mfma4(u32x2{a[2], a[3]}, u32x2{pb[kb][h][2], pb[kb][h][3]}, aux);
+        if constexpr (WCHK) {
+          const u32x4 aw4 =
+              *reinterpret_cast<const u32x4*>(&svsm[vsm_roww][32 * kb + 16 * h + 8 * grp]);
+          auxw = mfma4(u32x2{aw4[0], aw4[1]}, u32x2{pb[kb][h][0], pb[kb][h][1]}, auxw);
+          auxw = mfma4(u32x2{aw4[2], aw4[3]}, u32x2{pb[kb][h][2], pb[kb][h][3]}, auxw);
+        }
       }
     if constexpr (INJECT) {
       // C and L sites (checker state): a part of the fp32 accumulator pair
@@ -608,7 +656,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
             grp == 0) {
           const int el = fd.site == 5 ? fd.col : 2;   // c: hi (0) or lo (1) part
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
+          for (int i = 0; i < 4; ++i)
             if (i == el) aux[i] = __uint_as_float(__float_as_uint(aux[i]) ^ (1u << fd.bit));
         }
       }
@@ -797,7 +845,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     // exponent reference m (exp2 domain)
     const float l_p = sum_xor32(aux[2]);
     const float c_p = sum_xor32(aux[0] + aux[1]);
-    const float cw_p = WCHK ? sum_xor32(aux[4] + aux[5]) : 0.f;
+    const float cw_p = WCHK ? sum_xor32(auxw[0] + auxw[1]) : 0.f;
     if (qrow < Lq) {
       float* rec = p.ws + (((size_t)bh * Lq + qrow) * p.nsplit + split) * (D + 4);
       if (grp == 0) *reinterpret_cast<f32x4*>(rec) = f32x4{m2_run, l_p, c_p, cw_p};
@@ -858,7 +906,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     float sc_lhs = 0.f, sc_rhs = 0.f, sc_bound = 0.f;   // score check (debug outputs)
     if constexpr (WCHK) {
       act_w = sum_xor32(act_w);
-      pred_w = sum_xor32(aux[4] + aux[5]) * inv;
+      pred_w = sum_xor32(auxw[0] + auxw[1]) * inv;
       const float rw = pred_w - act_w;
       nonfinite = nonfinite || nonfinite_bits(rw);
       if (!(__builtin_fabsf(rw) <= p.tau_rel * (absum + __builtin_fabsf(pred_w)) + p.tau_abs)) f |= 4;
@@ -1087,7 +1135,7 @@ __global__ __launch_bounds__(kGThreads) void global_check_kernel(
   const uint16_t* ob = o + (size_t)bh * Lq * d;
   double sr = 0.0, sa = 0.0;
   for (int i = tid; i < Lq; i += kGThreads) sr += (double)r[i];
-  // O as 8-element chunks (rows are 16-byte aligned: d is 64, 96 or 128)
+  // O as 8-element chunks (rows are 16-byte aligned: d is 64, 96, 128 or 256)
   const size_t nchunk = (size_t)Lq * d / 8;
   for (size_t c = tid; c < nchunk; c += kGThreads) {
     const u32x4 w = *reinterpret_cast<const u32x4*>(ob + 8 * c);

@@ -125,6 +125,9 @@ def test_summary_counts(tmp_path):
     lo, hi = s["headline"]["wilson95"]
     assert lo < 2 / 3 < hi
     assert s["false_positives"] == 1
+    # with S counted: detected 2 of the 4 significant exponent flips
+    assert s["headline_with_S"]["detected"] == 2 and s["headline_with_S"]["silent"] == 2
+    assert s["S_exponent"]["silent"] == 1 and s["S_exponent"]["detected"] == 0
     assert s["per_site"]["S"]["silent"] == 1
     assert s["per_bit"]["O30"]["detected"] == 1
 

@@ -78,7 +78,11 @@ def brute(q, k, v, causal, scale, fault, key_tile, query_tile, exact=False, fact
         qi = list(q[i])
         ref = -math.inf
         o = [0.0] * d
-        l = chi = clo = 0.0
+        # c and l in two partial sums: keys with k mod 16 < 8 (half 0) and
+        # the rest (half 1); the C and L sites flip half 0
+        l = [0.0, 0.0]
+        chi = [0.0, 0.0]
+        clo = [0.0, 0.0]
         for t in range(last_t + 1):
             if site == "Q" and i == fault.row and t == fault.tile:
                 x = qi[fault.col]
@@ -101,7 +105,7 @@ def brute(q, k, v, causal, scale, fault, key_tile, query_tile, exact=False, fact
             if new != ref and ref != -math.inf:
                 a = 2.0 ** (ref - new)
                 o = [x * a for x in o]
-                l, chi, clo = l * a, chi * a, clo * a
+                l, chi, clo = [x * a for x in l], [x * a for x in chi], [x * a for x in clo]
             ref = new
             p = {}
             for kk in keys:
@@ -120,9 +124,10 @@ def brute(q, k, v, causal, scale, fault, key_tile, query_tile, exact=False, fact
                         h = xn
                     else:
                         lw = xn
-                l += p[kk]
-                chi += p[kk] * h
-                clo += p[kk] * lw
+                hf = 0 if kk % 16 < 8 else 1
+                l[hf] += p[kk]
+                chi[hf] += p[kk] * h
+                clo[hf] += p[kk] * lw
             for kk in keys:
                 w = p[kk]
                 if site == "P" and i == fault.row and kk == fault.col:
@@ -140,19 +145,20 @@ def brute(q, k, v, causal, scale, fault, key_tile, query_tile, exact=False, fact
                     site_x[0] = f32(x)
                     o[fault.col] = x * factor if exact else f32_flip(f32(x), fault.bit)
                 elif site == "C":
-                    x = chi if fault.col == 0 else clo
+                    x = chi[0] if fault.col == 0 else clo[0]
                     site_x[0] = f32(x)
                     xn = x * factor if exact else f32_flip(f32(x), fault.bit)
                     if fault.col == 0:
-                        chi = xn
+                        chi[0] = xn
                     else:
-                        clo = xn
+                        clo[0] = xn
                 elif site == "L":
-                    site_x[0] = f32(l)
-                    l = l * factor if exact else f32_flip(f32(l), fault.bit)
-        inv = 1.0 / l if l > 0 else 0.0
+                    site_x[0] = f32(l[0])
+                    l[0] = l[0] * factor if exact else f32_flip(f32(l[0]), fault.bit)
+        lt = l[0] + l[1]
+        inv = 1.0 / lt if lt > 0 else 0.0
         O = [x * inv for x in o]
-        out.append((O, (chi + clo) * inv, sum(O)))
+        out.append((O, (chi[0] + chi[1] + clo[0] + clo[1]) * inv, sum(O)))
     return out, site_x[0]
 
 
@@ -301,8 +307,9 @@ def test_site_values_match_the_brute_force_bit_for_bit(causal):
                 vis = FM._visible(i, 37, 45, causal)
                 vs, hi, lo = FM._sumrow_parts(v)
                 fr = FM.row_frame(k @ q[i], vis, FM.exp2_scale(scale), v, hi, lo, KT)
-                mv = {"O": fr["o"][t][1], "C": fr["c_hi"][t] if col == 0 else fr["c_lo"][t],
-                      "L": fr["l"][t]}[site]
+                mv = {"O": fr["o"][t][1],
+                      "C": fr["c_hi_half"][t] if col == 0 else fr["c_lo_half"][t],
+                      "L": fr["l_half"][t]}[site]
                 assert float(np.float32(mv)) == x, (site, i, t)
 
 
