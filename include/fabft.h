@@ -238,6 +238,22 @@ int fabft_global_check(const void* o, const float* resid, int B, int H, int Lq,
 void fabft_set_weighted_check(int on);
 int fabft_get_weighted_check(void);
 
+/*
+ * Persistent workgroups (a launch shape, not part of the method; default:
+ * on). With it on, fabft_attn_fwd and fabft_attn_fwd_nocheck launch only as
+ * many workgroups as the device holds at once (one per compute unit, two at
+ * d = 64) when there are more (head, query tile) items than that, each
+ * workgroup running a fixed list of items; the next item's Q and first key
+ * tiles load while the current item's last tiles and its epilogue run. It
+ * applies without the mask, or with it when B * H is a multiple of 8, and
+ * never to the split, debug, injection or score-check paths. Results are
+ * bitwise the same either way (each row is computed by the same
+ * instructions in the same order). 0 turns it off: one workgroup per item.
+ * Process-global, not thread-safe.
+ */
+void fabft_set_persistent(int on);
+int fabft_get_persistent(void);
+
 /* Number of keys per key tile of the kernel for head dimension d (the unit
  * of fabft_fault.tile at the O site), or FABFT_E_HEADDIM. */
 int fabft_key_tile(int d);

@@ -110,6 +110,10 @@ def _load() -> ctypes.CDLL:
     L.fabft_set_weighted_check.restype = None
     L.fabft_get_weighted_check.argtypes = []
     L.fabft_get_weighted_check.restype = _i
+    L.fabft_set_persistent.argtypes = [_i]
+    L.fabft_set_persistent.restype = None
+    L.fabft_get_persistent.argtypes = []
+    L.fabft_get_persistent.restype = _i
     L.fabft_key_tile.argtypes = [_i]
     L.fabft_key_tile.restype = _i
     L.fabft_query_tile.argtypes = [_i]
@@ -128,6 +132,7 @@ EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
            "fabft_set_stream", "fabft_set_threshold", "fabft_get_threshold",
            "fabft_global_check", "fabft_recompute_flagged",
            "fabft_set_weighted_check", "fabft_get_weighted_check",
+           "fabft_set_persistent", "fabft_get_persistent",
            "fabft_key_tile", "fabft_query_tile", "fabft_status_str")
 
 
@@ -199,6 +204,16 @@ def set_weighted_check(on: bool):
 
 def get_weighted_check() -> bool:
     return bool(_load().fabft_get_weighted_check())
+
+
+def set_persistent(on: bool):
+    """Persistent workgroups for attn_fwd (process-global, default on): a
+    launch shape only, the results are bitwise the same."""
+    _load().fabft_set_persistent(int(bool(on)))
+
+
+def get_persistent() -> bool:
+    return bool(_load().fabft_get_persistent())
 
 
 def key_tile(d: int) -> int:
@@ -489,6 +504,7 @@ __all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_debug", "attn_fwd_splitkv", 
            "splitkv_default_splits",
            "global_check", "recompute_flagged", "Fault", "FabftError", "set_threshold",
            "set_score_check", "score_check_workspace_bytes", "get_score_threshold",
-           "get_threshold", "set_weighted_check", "get_weighted_check", "key_tile",
+           "get_threshold", "set_weighted_check", "get_weighted_check", "set_persistent",
+           "get_persistent", "key_tile",
            "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "MAX_FAULTS", "FLAG_RESID",
            "FLAG_NONFINITE", "FLAG_WEIGHTED", "FLAG_SCORES"]

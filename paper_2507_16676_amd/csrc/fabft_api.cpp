@@ -94,7 +94,9 @@ fabft::FwdParams make_params(const void* q, const void* k, const void* v, void* 
   p.Lq = Lq;
   p.Lk = Lk;
   p.n_qt = n_qt;
+  p.n_items = grid;
   p.grid = grid;
+  p.persist = 0;
   // A masked score is -inf and enters exp2 as -inf * sl2: sl2 must not be
   // zero. Raised to 2^-126 (only scale 0 or a subnormal one is), it changes
   // no exponential of a score below 2^100 in magnitude (s * sl2 < 2^-26 rounds
@@ -439,6 +441,10 @@ int fabft_set_score_check(void* workspace, long long workspace_bytes, float tau_
 float fabft_get_score_threshold(void) { return g_tau_s; }
 
 int fabft_get_weighted_check(void) { return g_wcheck; }
+
+void fabft_set_persistent(int on) { fabft::set_persistent(on != 0); }
+
+int fabft_get_persistent(void) { return fabft::get_persistent() ? 1 : 0; }
 
 int fabft_key_tile(int d) {
   if (!head_dim_ok(d)) return FABFT_E_HEADDIM;

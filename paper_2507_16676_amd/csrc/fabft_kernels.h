@@ -53,7 +53,11 @@ struct FwdParams {
   float tau_s;
   int Lq, Lk;
   int n_qt;       // query tiles per head
-  int grid;       // workgroups = B * H * n_qt
+  int n_items;    // work items (head, query tile): B * H * n_qt
+  int grid;       // workgroups: n_items (times nsplit in mode 3), or fewer
+                  // with persist
+  int persist;    // 1: each of the grid's workgroups runs a list of items
+                  // (set by launch_fwd, modes 0 and 1 only)
   float sl2;      // scale * log2(e)
   float tau_rel, tau_abs;
   int nf;                          // faults in f (injection kernels only)
@@ -61,8 +65,13 @@ struct FwdParams {
 };
 
 // mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection,
-// 3: checksum on, one key split per workgroup (partial states to p.ws)
+// 3: checksum on, one key split per workgroup (partial states to p.ws).
+// Modes 0 and 1 (without the score check) run as many workgroups as fit on
+// the device at once, each running a list of items, when there are more
+// items than that and set_persistent has not turned it off.
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream);
+void set_persistent(bool on);
+bool get_persistent();
 int key_tile(int d);
 // Width the kernels compute with for a head dimension d (64, 96, 128 or
 // 256): d itself, or 128 for d = 96 (columns 96..127 are zero on chip).

@@ -62,6 +62,7 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
 #include <climits>
 
 #include "fabft_kernels.h"
@@ -252,6 +253,78 @@ struct Ring {
   uint16_t vsm[Cfg<D>::STAGES][kVsmRows][VS];
 };
 
+// ---- work items: (head bh, query tile qt) pairs, p.n_items of them.
+// Item of block vb when each workgroup runs one item. Workgroups go to the 8
+// XCDs round robin (XCD = id mod 8). Without a mask every item costs the
+// same: each XCD takes a contiguous range of heads, so that a head's K and V
+// stay in one L2. With the causal mask the work of a query tile grows with
+// its index: the heaviest tiles go first (longest job first), a band of
+// heads at a time, and with a head count divisible by 8 a head stays on one
+// XCD.
+template <bool CAUSAL>
+__device__ __forceinline__ void item_of_block(const FwdParams& p, int vb, int& bh, int& qt) {
+  const int G = p.n_items;
+  if (CAUSAL) {
+    const int BH = G / p.n_qt;
+    if ((BH & 7) == 0) {
+      // XCD x owns heads x, x + 8, ...; it runs them a band of heads at a
+      // time, each band longest tile first. The query tiles of a band stream
+      // the same few K/V tiles at about the same time, so one HBM read
+      // serves several of them from L2. A band holds as few heads as still
+      // give the XCD's 32 CUs at least 64 query tiles (at most kCausalBand):
+      // with long rows one head suffices, and all of an XCD's tiles then
+      // share one head's K/V.
+      const int bandw = min(kCausalBand, max(1, (64 + p.n_qt - 1) / p.n_qt));
+      const int xcd = vb & 7, slot = vb >> 3;
+      const int band = slot / (bandw * p.n_qt);
+      const int h0 = band * bandw;
+      const int nb = min(bandw, (BH >> 3) - h0);
+      const int w = slot - h0 * p.n_qt;
+      const int qr = w / nb;
+      bh = (h0 + w - qr * nb) * 8 + xcd;
+      qt = p.n_qt - 1 - qr;
+    } else {
+      const int qr = vb / BH;
+      bh = vb - qr * BH;
+      qt = p.n_qt - 1 - qr;
+    }
+  } else {
+    const int xcd = vb & 7;
+    const int per = G >> 3, rem = G & 7;
+    const int slot = vb >> 3;
+    const int logical = (xcd < rem) ? xcd * (per + 1) + slot
+                                    : rem * (per + 1) + (xcd - rem) * per + slot;
+    bh = logical / p.n_qt;
+    qt = logical - bh * p.n_qt;
+  }
+}
+
+// Item k of workgroup b when p.grid workgroups (a multiple of 8, one or two
+// per CU) each run a list of items; false past the end of b's list.
+// Workgroup b runs on XCD b mod 8 and takes only that XCD's items, in the
+// one-item order (slot by slot): the XCD's G/8 workgroups deal its slots in
+// rounds of G/8, every other round in reverse order. With the mask the slots
+// of a band come heaviest first, so a workgroup's heavy tile of one round
+// meets a light one in the next and the workgroups get about the same number
+// of key tiles; the band's heads are still the ones in flight (the host takes
+// this path with the mask only for a head count divisible by 8).
+template <bool CAUSAL>
+__device__ __forceinline__ bool persistent_item(const FwdParams& p, int b, int k, int& bh,
+                                                int& qt) {
+  const int G = p.grid;
+  if (!CAUSAL) {
+    const long long vb = (long long)b + (long long)k * G;
+    if (vb >= p.n_items) return false;
+    item_of_block<false>(p, (int)vb, bh, qt);
+    return true;
+  }
+  const int nw = G >> 3, wx = b >> 3;
+  const long long slot = (long long)k * nw + ((k & 1) ? nw - 1 - wx : wx);
+  if (slot >= (p.n_items >> 3)) return false;
+  item_of_block<true>(p, (int)(slot * 8 + (b & 7)), bh, qt);
+  return true;
+}
+
 template <int S>
 struct StageId {
   static constexpr int value = S;
@@ -274,6 +347,10 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   constexpr int NDS = D / 16;     // 16-wide steps over d in Q K^T
   constexpr int NLD = BC * CPR / kThreads;   // 16-byte loads per thread per tensor and tile
   static_assert(NLD >= 1 && BC * CPR == NLD * kThreads, "loads cover the tile");
+  // a workgroup may run a list of items (p.persist), handing the LDS ring
+  // from one item to the next: the next item's Q and first key tiles load
+  // while the current item's last tiles and epilogue run
+  constexpr bool kPersist = !INJECT && !SPLIT && !SCHK && Cfg<D>::AHEAD >= 3;
 
   __shared__ __attribute__((aligned(16))) Ring<D> ring;
 
@@ -283,97 +360,89 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   const int mrow = lane & 31;   // MFMA row / column index of this lane
   const int grp = lane >> 5;    // which 8-wide k slice this lane holds
 
-  // ---- workgroup -> (head, query tile). Workgroups go to the 8 XCDs round
-  // robin (XCD = id mod 8). Without a mask every tile costs the same: each
-  // XCD takes a contiguous range of heads, so that a head's K and V stay in
-  // one L2. With the causal mask the work per query tile grows with its
-  // index: the heaviest tiles go first (longest job first), a band of heads
-  // at a time, and with a head count divisible by 8 a head stays on one XCD.
-  const int G = p.grid;
+  // ---- this workgroup's first item
   const int bid = blockIdx.x;
-  int bh, qt, split = 0;
-  if (SPLIT) {
+  int bh = 0, qt = 0, split = 0;
+  if constexpr (SPLIT) {
     // the splits of one (head, query tile) are neighbours
     split = bid % p.nsplit;
     const int lg = bid / p.nsplit;
     bh = lg / p.n_qt;
     qt = lg - bh * p.n_qt;
-  } else if (CAUSAL) {
-    const int BH = G / p.n_qt;
-    if ((BH & 7) == 0) {
-      // XCD x owns heads x, x + 8, ...; it runs them a band of heads at a
-      // time, each band longest tile first. The query tiles of a band stream
-      // the same few K/V tiles at about the same time, so one HBM read
-      // serves several of them from L2. A band holds as few heads as still
-      // give the XCD's 32 CUs at least 64 query tiles (at most kCausalBand):
-      // with long rows one head suffices, and all of an XCD's tiles then
-      // share one head's K/V.
-      const int bandw = min(kCausalBand, max(1, (64 + p.n_qt - 1) / p.n_qt));
-      const int xcd = bid & 7, slot = bid >> 3;
-      const int band = slot / (bandw * p.n_qt);
-      const int h0 = band * bandw;
-      const int nb = min(bandw, (BH >> 3) - h0);
-      const int w = slot - h0 * p.n_qt;
-      const int qr = w / nb;
-      bh = (h0 + w - qr * nb) * 8 + xcd;
-      qt = p.n_qt - 1 - qr;
-    } else {
-      const int qr = bid / BH;
-      bh = bid - qr * BH;
-      qt = p.n_qt - 1 - qr;
-    }
+  } else if (kPersist && p.persist) {
+    if (!persistent_item<CAUSAL>(p, bid, 0, bh, qt)) return;   // nothing to do
   } else {
-    const int xcd = bid & 7;
-    const int per = G >> 3, rem = G & 7;
-    const int slot = bid >> 3;
-    const int logical = (xcd < rem) ? xcd * (per + 1) + slot
-                                    : rem * (per + 1) + (xcd - rem) * per + slot;
-    bh = logical / p.n_qt;
-    qt = logical - bh * p.n_qt;
+    item_of_block<CAUSAL>(p, bid, bh, qt);
   }
+  // wave-uniform (for the compiler's divergence analysis: scalar registers)
+  bh = __builtin_amdgcn_readfirstlane(bh);
+  qt = __builtin_amdgcn_readfirstlane(qt);
 
   const int Lq = p.Lq, Lk = p.Lk;
-  const int q0 = qt * kBr;
   const int off = Lk - Lq;
   // q, k, v, o rows hold DIO <= D columns in memory; on chip the rows are D
   // wide and columns DIO.. are zero (zero scores, zero outputs)
   const int DIO = p.dio;
   const int CIO = DIO / 8;   // 16-byte chunks per row in memory
-  const size_t qbase = (size_t)bh * (size_t)Lq * DIO;
-  const size_t kbase = (size_t)bh * (size_t)Lk * DIO;
+  const uint32_t kv_bytes = (uint32_t)Lk * DIO * 2;
+  // key tiles of query tile qt_ (keys [0, kend)); wave-uniform (the
+  // division runs on the vector ALU): scalar branches
+  auto tiles_of = [&](int qt_) {
+    int kend = Lk;
+    if (CAUSAL) kend = min(Lk, qt_ * kBr + kBr + off);
+    return __builtin_amdgcn_readfirstlane(kend > 0 ? (kend + BC - 1) / BC : 0);
+  };
 
-  int kend = Lk;
-  if (CAUSAL) kend = min(Lk, q0 + kBr + off);
-  // wave-uniform (the division runs on the vector ALU): scalar branches
-  const int ntiles = __builtin_amdgcn_readfirstlane(kend > 0 ? (kend + BC - 1) / BC : 0);
-  // key tiles [t_lo, t_end) of this workgroup
-  int t_lo = 0, t_end = ntiles;
-  if (SPLIT) {
-    t_lo = min(ntiles, split * p.split_tiles);
-    t_end = min(ntiles, t_lo + p.split_tiles);
-  }
-
-  const int wq_lo = q0 + 32 * wave;  // first query row of this wave
-  const int qrow = wq_lo + mrow;
+  // ---- the current item: key tiles [t_lo, t_end), this wave's first query
+  // row wq_lo, the lane's row qrow, and the head's K / V buffer resources
+  int t_lo = 0, t_end = 0, wq_lo = 0, qrow = 0;
+  size_t qbase = 0;
+  i32x4 krs, vrs;
+  auto set_item = [&]() {
+    const int ntiles = tiles_of(qt);
+    t_lo = 0;
+    t_end = ntiles;
+    if (SPLIT) {
+      t_lo = min(ntiles, split * p.split_tiles);
+      t_end = min(ntiles, t_lo + p.split_tiles);
+    }
+    wq_lo = qt * kBr + 32 * wave;
+    qrow = wq_lo + mrow;
+    qbase = (size_t)bh * (size_t)Lq * DIO;
+    const size_t kbase = (size_t)bh * (size_t)Lk * DIO;
+    krs = buffer_rsrc(p.k + kbase, kv_bytes);
+    vrs = buffer_rsrc(p.v + kbase, kv_bytes);
+  };
+  set_item();
+  // ---- the next item of a persistent workgroup: head, query tile, key
+  // tiles, K / V resources; cont: its first AHEAD tiles go into the ring
+  // during the current item's last tiles (the current item has a multiple of
+  // kStages tiles, so the next one starts in stage 0); te_v: the end of the
+  // tiles in flight, for the waits
+  int nbh = 0, nqt = 0, n_tend = 0, te_v = 0;
+  bool cont = false;
+  i32x4 krsN = {}, vrsN = {};
 
   // ---- Q fragments (B operand): lane holds query qrow, d slice 8*grp
   u32x4 qf[NDS];
+  auto load_q = [&](int bh_, int qt_) __attribute__((always_inline)) {
+    const int r = qt_ * kBr + 32 * wave + mrow;
+    const uint16_t* qr = p.q + (size_t)bh_ * (size_t)Lq * DIO + (size_t)r * DIO;
 #pragma unroll
-  for (int s = 0; s < NDS; ++s) {
-    qf[s] = u32x4{0, 0, 0, 0};
-    if (qrow < Lq && 2 * s + grp < CIO)
-      qf[s] = *reinterpret_cast<const u32x4*>(p.q + qbase + (size_t)qrow * DIO + 16 * s + 8 * grp);
-  }
+    for (int s = 0; s < NDS; ++s) {
+      qf[s] = u32x4{0, 0, 0, 0};
+      if (r < Lq && 2 * s + grp < CIO) qf[s] = *reinterpret_cast<const u32x4*>(qr + 16 * s + 8 * grp);
+    }
+  };
+  load_q(bh, qt);
 
   f32x16 oacc[NDB];
-#pragma unroll
-  for (int b = 0; b < NDB; ++b) oacc[b] = f32x16{};
   // c / l accumulator of this lane's query: [0] c_hi, [1] c_lo, [2] l over
   // the lane's half of the keys (4x4x4 products; the two halves add up at
   // the end); with the weighted check, auxw [0] c_w hi, [1] c_w lo alike
-  f32x4 aux = {}, auxw = {};
-  float s_lhs = 0.f;                  // score check: sum of this lane's scores in full tiles
-  float m2_run = -__builtin_inff();   // running max, exp2 domain (s * scale * log2 e)
+  f32x4 aux, auxw;
+  float s_lhs;    // score check: sum of this lane's scores in full tiles
+  float m2_run;   // running max, exp2 domain (s * scale * log2 e)
   const float sl2 = p.sl2;
 
   // constant rows of the c / l operand in every stage (visible after the
@@ -395,9 +464,6 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   // ---- loader: 16-byte slot j*512 + tid of a tile holds row slot/CPR, stored
   // chunk slot%CPR (logical chunk = stored ^ swz(row)); rows past Lk read as
   // zeros (the mask gives them weight 0)
-  const uint32_t kv_bytes = (uint32_t)Lk * DIO * 2;
-  const i32x4 krs = buffer_rsrc(p.k + kbase, kv_bytes);
-  const i32x4 vrs = buffer_rsrc(p.v + kbase, kv_bytes);
   uint32_t kvo[NLD], vvo[NLD];
 #pragma unroll
   for (int j = 0; j < NLD; ++j) {
@@ -414,7 +480,18 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   const uint32_t wave_lds = __builtin_amdgcn_readfirstlane(ring_lds + 1024u * wave);
   auto issue = [&](auto S_, int t) {
     constexpr int S = decltype(S_)::value;
-    if (t >= t_end) return;
+    i32x4 kr = krs, vr = vrs;
+    if (t >= t_end) {
+      if constexpr (!kPersist) {
+        return;
+      } else {
+        // tile t - t_end of the next item (into the stage it starts in)
+        t -= t_end;
+        if (!cont || t >= n_tend) return;
+        kr = krsN;
+        vr = vrsN;
+      }
+    }
     const uint32_t soff = (uint32_t)t * BC * DIO * 2;
     // opaque copy: the destination addresses are formed here from one SGPR
     // (scalar adds) rather than hoisted as one live SGPR per stage and load
@@ -425,8 +502,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
       // each wave writes its own contiguous 1 KiB of the stage
       constexpr uint32_t kOff = offsetof(Ring<D>, k) + S * sizeof(Ring<D>::k[0]);
       constexpr uint32_t vOff = offsetof(Ring<D>, v) + S * sizeof(Ring<D>::v[0]);
-      buffer_load_lds16(krs, kvo[j], soff, wl + kOff + j * kThreads * 16);
-      buffer_load_lds16(vrs, vvo[j], soff, wl + vOff + j * kThreads * 16);
+      buffer_load_lds16(kr, kvo[j], soff, wl + kOff + j * kThreads * 16);
+      buffer_load_lds16(vr, vvo[j], soff, wl + vOff + j * kThreads * 16);
     }
   };
 
@@ -751,227 +828,315 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     }
     wait_vmcnt<0>();
   };
-  // tile t sits in stage (t - t_lo) % kStages; the loop below is unrolled
-  // kStages times so that each copy knows its stages at compile time. With
-  // three tiles ahead, sumrow of tile t+1 is taken at the end of step t
-  // (its loads are waited for at the top of step t); with one tile ahead,
-  // sumrow of tile t is taken in step t before the compute, behind a second
-  // barrier.
-  if (t_end > t_lo) {
-    issue(StageId<0>(), t_lo);
-    if constexpr (AHEAD >= 2) issue(StageId<1>(), t_lo + 1);
-    if constexpr (AHEAD >= 3) {
-      issue(StageId<2>(), t_lo + 2);
-      // first tile complete; the next two may be outstanding
-      wait_tiles(min(2, t_end - 1 - t_lo));
-      __syncthreads();
-      if constexpr (CHECK) sumrow(StageId<0>());
-    }
-  }
-  // A use of Q here, on every path into the loop, puts the compiler's own
-  // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
-  // also waits for the first tiles) before the loop rather than inside it.
-#pragma unroll
-  for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
-  static_assert(kStages == 4 || kStages == 2, "the loop below is unrolled over the stages");
-  static_assert(AHEAD == kStages - 1, "the stage of tile t-1 takes tile t+AHEAD");
-  auto step = [&](auto S_, int t) __attribute__((always_inline)) {
-    constexpr int S = decltype(S_)::value;
-    if constexpr (AHEAD >= 3) {
-      // tile t+1 complete (tile t+2 may still be in flight); after the
-      // barrier every wave is done with tile t-1, whose stage takes tile t+3
-      wait_tiles(min(1, t_end - 2 - t));
-      __syncthreads();
-    } else {
-      // tile t complete; after the barrier every wave is done with tile t-1,
-      // whose stage takes tile t+1, loading while tile t is processed
-      wait_tiles(0);
-      __syncthreads();
-      issue(StageId<(S + 1) % kStages>(), t + 1);
-      if constexpr (CHECK) {
-        sumrow(S_);
-        __syncthreads();
+  // ---- the items of this workgroup (one unless p.persist)
+  bool primed = false;   // the item's first tiles are already in the ring
+  for (int k = 0;; ++k) {
+    // tile t sits in stage (t - t_lo) % kStages; the loop below is unrolled
+    // kStages times so that each copy knows its stages at compile time. With
+    // three tiles ahead, sumrow of tile t+1 is taken at the end of step t
+    // (its loads are waited for at the top of step t); with one tile ahead,
+    // sumrow of tile t is taken in step t before the compute, behind a second
+    // barrier.
+    // the next item, and whether the ring passes to it
+    bool has_next = false;
+    cont = false;
+    te_v = t_end;
+    if constexpr (kPersist) {
+      if (p.persist) {
+        has_next = __builtin_amdgcn_readfirstlane(
+                       (int)persistent_item<CAUSAL>(p, bid, k + 1, nbh, nqt)) != 0;
+      }
+      if (has_next) {
+        nbh = __builtin_amdgcn_readfirstlane(nbh);
+        nqt = __builtin_amdgcn_readfirstlane(nqt);
+        n_tend = tiles_of(nqt);
+        cont = t_end > t_lo && (t_end - t_lo) % kStages == 0;
+        if (cont) {
+          te_v = t_end + min(AHEAD, n_tend);
+          const size_t kb = (size_t)nbh * (size_t)Lk * DIO;
+          krsN = buffer_rsrc(p.k + kb, kv_bytes);
+          vrsN = buffer_rsrc(p.v + kb, kv_bytes);
+        }
       }
     }
-    if constexpr (INJECT) {
-      // V site: flip a bit of V[row][col] in this workgroup's copy of the
-      // tile, after its sumrow was taken and before any wave reads it; VS
-      // site (checker state): the same for the tile's sumrow operand (col 0:
-      // hi part, col 1: lo part). The condition is uniform over the
-      // workgroup; faults apply one after another.
-      bool hit = false;
-      for (int fi = 0; fi < p.nf; ++fi) {
-        const FaultDesc fd = p.f[fi];
-        if ((fd.site == 4 || fd.site == 9) && bh == fd.bh && qt == fd.tile) {
-          const int key = fd.row - t * BC;
-          if (key >= 0 && key < BC) {
-            hit = true;
-            if (tid == 0) {
-              uint16_t* e = fd.site == 4
-                                ? ring.v[S] + Tile<D>::vidx(key, fd.col >> 3) + (fd.col & 7)
-                                : &ring.vsm[S][kRowVsHi + fd.col][key];
-              *e = (uint16_t)(*e ^ (1u << fd.bit));
+#pragma unroll
+    for (int b = 0; b < NDB; ++b) oacc[b] = f32x16{};
+    aux = f32x4{};
+    auxw = f32x4{};
+    s_lhs = 0.f;
+    m2_run = -__builtin_inff();
+    if (!primed && t_end > t_lo) {
+      // after a previous item whose ring drained, every wave must be done with
+      // its stages before they take new tiles
+      if (kPersist && k > 0) __syncthreads();
+      issue(StageId<0>(), t_lo);
+      if constexpr (AHEAD >= 2) issue(StageId<1>(), t_lo + 1);
+      if constexpr (AHEAD >= 3) {
+        issue(StageId<2>(), t_lo + 2);
+        // first tile complete; the next two may be outstanding
+        wait_tiles(min(2, t_end - 1 - t_lo));
+        __syncthreads();
+        if constexpr (CHECK) sumrow(StageId<0>());
+      }
+    }
+    // A use of Q here, on every path into the loop, puts the compiler's own
+    // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
+    // also waits for the first tiles) before the loop rather than inside it.
+#pragma unroll
+    for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
+    static_assert(kStages == 4 || kStages == 2, "the loop below is unrolled over the stages");
+    static_assert(AHEAD == kStages - 1, "the stage of tile t-1 takes tile t+AHEAD");
+    auto step = [&](auto S_, int t) __attribute__((always_inline)) {
+      constexpr int S = decltype(S_)::value;
+      if constexpr (AHEAD >= 3) {
+        // tile t+1 complete (tile t+2 may still be in flight); after the
+        // barrier every wave is done with tile t-1, whose stage takes tile t+3
+        wait_tiles(min(1, te_v - 2 - t));
+        __syncthreads();
+      } else {
+        // tile t complete; after the barrier every wave is done with tile t-1,
+        // whose stage takes tile t+1, loading while tile t is processed
+        wait_tiles(0);
+        __syncthreads();
+        issue(StageId<(S + 1) % kStages>(), t + 1);
+        if constexpr (CHECK) {
+          sumrow(S_);
+          __syncthreads();
+        }
+      }
+      if constexpr (INJECT) {
+        // V site: flip a bit of V[row][col] in this workgroup's copy of the
+        // tile, after its sumrow was taken and before any wave reads it; VS
+        // site (checker state): the same for the tile's sumrow operand (col 0:
+        // hi part, col 1: lo part). The condition is uniform over the
+        // workgroup; faults apply one after another.
+        bool hit = false;
+        for (int fi = 0; fi < p.nf; ++fi) {
+          const FaultDesc fd = p.f[fi];
+          if ((fd.site == 4 || fd.site == 9) && bh == fd.bh && qt == fd.tile) {
+            const int key = fd.row - t * BC;
+            if (key >= 0 && key < BC) {
+              hit = true;
+              if (tid == 0) {
+                uint16_t* e = fd.site == 4
+                                  ? ring.v[S] + Tile<D>::vidx(key, fd.col >> 3) + (fd.col & 7)
+                                  : &ring.vsm[S][kRowVsHi + fd.col][key];
+                *e = (uint16_t)(*e ^ (1u << fd.bit));
+              }
             }
           }
         }
+        if (hit) __syncthreads();
       }
-      if (hit) __syncthreads();
-    }
-    // waves whose rows see none of this tile's keys, or that hold no row
-    // below Lq, skip it (they still load and take sumrow for the others)
-    if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(S_, t);
-    if constexpr (AHEAD >= 3) {
-      issue(StageId<(S + 3) % kStages>(), t + 3);
-      if constexpr (CHECK) {
-        if (t + 1 < t_end) sumrow(StageId<(S + 1) % kStages>());
-      }
-    }
-  };
-  for (int t = t_lo; t < t_end; t += kStages) {
-    step(StageId<0>(), t);
-    if (t + 1 >= t_end) break;
-    step(StageId<1>(), t + 1);
-    if constexpr (kStages == 4) {
-      if (t + 2 >= t_end) break;
-      step(StageId<2 % kStages>(), t + 2);
-      if (t + 3 >= t_end) break;
-      step(StageId<3 % kStages>(), t + 3);
-    }
-  }
-
-  if constexpr (SPLIT) {
-    // ---- partial state of each row for this key split (merged by
-    // merge_kernel): m, l, c, c_w and the unnormalised o, in the same
-    // exponent reference m (exp2 domain)
-    const float l_p = sum_xor32(aux[2]);
-    const float c_p = sum_xor32(aux[0] + aux[1]);
-    const float cw_p = WCHK ? sum_xor32(auxw[0] + auxw[1]) : 0.f;
-    if (qrow < Lq) {
-      float* rec = p.ws + (((size_t)bh * Lq + qrow) * p.nsplit + split) * (D + 4);
-      if (grp == 0) *reinterpret_cast<f32x4*>(rec) = f32x4{m2_run, l_p, c_p, cw_p};
-#pragma unroll
-      for (int db = 0; db < NDB; ++db)
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-          *reinterpret_cast<f32x4*>(rec + 4 + 32 * db + 8 * a + 4 * grp) =
-              f32x4{oacc[db][4 * a], oacc[db][4 * a + 1], oacc[db][4 * a + 2], oacc[db][4 * a + 3]};
-    }
-    return;
-  }
-
-  // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
-  const float l_tot = sum_xor32(aux[2]);
-  const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
-  float act = 0.f, absum = 0.f, act_w = 0.f;
-#pragma unroll
-  for (int db = 0; db < NDB; ++db)
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float x = oacc[db][i] * inv;
-      oacc[db][i] = x;
-      act += x;
-      absum += __builtin_fabsf(x);
-      // column 32db + 8(i/4) + 4grp + i%4 is even iff i is even
-      act_w += (i & 1) ? -x : x;
-    }
-  if (qrow < Lq) {
-    uint16_t* orow = p.o + qbase + (size_t)qrow * DIO;
-#pragma unroll
-    for (int db = 0; db < NDB; ++db) {
-      if (32 * db >= DIO) break;   // DIO is a multiple of 32
-#pragma unroll
-      for (int a = 0; a < 4; ++a) {
-        const u32x2 w = {pack_bf16x2(oacc[db][4 * a], oacc[db][4 * a + 1]),
-                         pack_bf16x2(oacc[db][4 * a + 2], oacc[db][4 * a + 3])};
-        *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * a + 4 * grp) = w;
-      }
-    }
-  }
-  if constexpr (CHECK) {
-    act = sum_xor32(act);
-    absum = sum_xor32(absum);
-    const float c_tot = sum_xor32(aux[0] + aux[1]);
-    const float pred = c_tot * inv;
-    const float r = pred - act;
-    const float M = absum + __builtin_fabsf(pred);
-    // non-finite test on the bits (this file is built with relaxed NaN rules);
-    // a non-finite residual also fails the threshold comparison. An overflow
-    // of sum_j |O_ij| (a huge but finite row) would make the threshold
-    // infinite and pass any residual, so it counts as non-finite as well.
-    bool nonfinite = nonfinite_bits(r) || nonfinite_bits(absum);
-    uint8_t f = (__builtin_fabsf(r) <= p.tau_rel * M + p.tau_abs) ? 0 : 1;
-    // weighted check: pred_w = c_w / l against sum_j (-1)^j O_ij (the same
-    // threshold rule; |w_j| = 1 keeps M)
-    float pred_w = 0.f;
-    float sc_lhs = 0.f, sc_rhs = 0.f, sc_bound = 0.f;   // score check (debug outputs)
-    if constexpr (WCHK) {
-      act_w = sum_xor32(act_w);
-      pred_w = sum_xor32(auxw[0] + auxw[1]) * inv;
-      const float rw = pred_w - act_w;
-      nonfinite = nonfinite || nonfinite_bits(rw);
-      if (!(__builtin_fabsf(rw) <= p.tau_rel * (absum + __builtin_fabsf(pred_w)) + p.tau_abs)) f |= 4;
-    }
-    if constexpr (SCHK) {
-      // score check: sum over the full key tiles of s_ij against
-      // q_i . sum_k K_k over the same keys (the prefix of the K column sums
-      // up to the wave's first masked tile), within tau_s * |q_i| . sum_k |K_k|
-      int tw = Lk / BC;   // tiles without the key-range mask
-      if (CAUSAL) {
-        const int lim = wq_lo + off + 1;   // tiles wholly below the wave's diagonal
-        tw = min(tw, lim <= 0 ? 0 : lim / BC);
-      }
-      const size_t kro = ((size_t)bh * (p.ntk + 1) + tw) * D;
-      float rhs = 0.f, ms = 0.f;
-#pragma unroll
-      for (int s2 = 0; s2 < NDS; ++s2) {
-        const int c0 = 16 * s2 + 8 * grp;   // the lane's 8 columns of q
-        const f32x4 kp0 = *reinterpret_cast<const f32x4*>(p.kpre + kro + c0);
-        const f32x4 kp1 = *reinterpret_cast<const f32x4*>(p.kpre + kro + c0 + 4);
-        const f32x4 ka0 = *reinterpret_cast<const f32x4*>(p.kabs + kro + c0);
-        const f32x4 ka1 = *reinterpret_cast<const f32x4*>(p.kabs + kro + c0 + 4);
-        const float kp[8] = {kp0[0], kp0[1], kp0[2], kp0[3], kp1[0], kp1[1], kp1[2], kp1[3]};
-        const float ka[8] = {ka0[0], ka0[1], ka0[2], ka0[3], ka1[0], ka1[1], ka1[2], ka1[3]};
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float qa = __uint_as_float(qf[s2][e] << 16);
-          const float qb = __uint_as_float(qf[s2][e] & 0xffff0000u);
-          rhs = __builtin_fmaf(qa, kp[2 * e], __builtin_fmaf(qb, kp[2 * e + 1], rhs));
-          ms = __builtin_fmaf(__builtin_fabsf(qa), ka[2 * e],
-                              __builtin_fmaf(__builtin_fabsf(qb), ka[2 * e + 1], ms));
+      // waves whose rows see none of this tile's keys, or that hold no row
+      // below Lq, skip it (they still load and take sumrow for the others)
+      if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(S_, t);
+      if constexpr (AHEAD >= 3) {
+        issue(StageId<(S + 3) % kStages>(), t + 3);
+        if constexpr (CHECK) {
+          if (t + 1 < te_v) sumrow(StageId<(S + 1) % kStages>());
         }
       }
-      // scores carry the softmax scale only in the exponent (exp2 of s * sl2):
-      // the sums compare raw q . k
-      const float lhs = sum_xor32(s_lhs);
-      rhs = sum_xor32(rhs);
-      ms = sum_xor32(ms);
-      const float rs = lhs - rhs;
-      nonfinite = nonfinite || nonfinite_bits(rs);
-      if (!(__builtin_fabsf(rs) <= p.tau_s * ms + p.tau_abs)) f |= 8;
-      sc_lhs = lhs;
-      sc_rhs = rhs;
-      sc_bound = ms;
-    }
-    if (nonfinite) f |= 3;
-    if (grp == 0 && qrow < Lq) {
-      const size_t ri = (size_t)bh * Lq + qrow;
-      p.resid[ri] = r;
-      p.flags[ri] = f;
-      if constexpr (INJECT) {
-        if (p.pred) p.pred[ri] = pred;
-        if (p.actual) p.actual[ri] = act;
-        if (p.pred_w) p.pred_w[ri] = pred_w;
-        if (p.actual_w) p.actual_w[ri] = WCHK ? act_w : 0.f;
-        if (p.s_lhs) p.s_lhs[ri] = sc_lhs;
-        if (p.s_rhs) p.s_rhs[ri] = sc_rhs;
-        if (p.s_bound) p.s_bound[ri] = sc_bound;
+    };
+    for (int t = t_lo; t < t_end; t += kStages) {
+      step(StageId<0>(), t);
+      if (t + 1 >= t_end) break;
+      step(StageId<1>(), t + 1);
+      if constexpr (kStages == 4) {
+        if (t + 2 >= t_end) break;
+        step(StageId<2 % kStages>(), t + 2);
+        if (t + 3 >= t_end) break;
+        step(StageId<3 % kStages>(), t + 3);
       }
     }
+    // the next item's Q loads while this item's epilogue runs (q is not read
+    // after the last Q K^T)
+    if constexpr (kPersist) {
+      if (cont) load_q(nbh, nqt);
+    }
+
+    if constexpr (SPLIT) {
+      // ---- partial state of each row for this key split (merged by
+      // merge_kernel): m, l, c, c_w and the unnormalised o, in the same
+      // exponent reference m (exp2 domain)
+      const float l_p = sum_xor32(aux[2]);
+      const float c_p = sum_xor32(aux[0] + aux[1]);
+      const float cw_p = WCHK ? sum_xor32(auxw[0] + auxw[1]) : 0.f;
+      if (qrow < Lq) {
+        float* rec = p.ws + (((size_t)bh * Lq + qrow) * p.nsplit + split) * (D + 4);
+        if (grp == 0) *reinterpret_cast<f32x4*>(rec) = f32x4{m2_run, l_p, c_p, cw_p};
+#pragma unroll
+        for (int db = 0; db < NDB; ++db)
+#pragma unroll
+          for (int a = 0; a < 4; ++a)
+            *reinterpret_cast<f32x4*>(rec + 4 + 32 * db + 8 * a + 4 * grp) =
+                f32x4{oacc[db][4 * a], oacc[db][4 * a + 1], oacc[db][4 * a + 2], oacc[db][4 * a + 3]};
+      }
+      return;
+    }
+
+    // ---- epilogue: O = o / l (Alg. 3), pred = c / l (Eq. 8), check
+    const float l_tot = sum_xor32(aux[2]);
+    const float inv = l_tot > 0.f ? 1.0f / l_tot : 0.f;
+    float act = 0.f, absum = 0.f, act_w = 0.f;
+#pragma unroll
+    for (int db = 0; db < NDB; ++db)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float x = oacc[db][i] * inv;
+        oacc[db][i] = x;
+        act += x;
+        absum += __builtin_fabsf(x);
+        // column 32db + 8(i/4) + 4grp + i%4 is even iff i is even
+        act_w += (i & 1) ? -x : x;
+      }
+    if (qrow < Lq) {
+      uint16_t* orow = p.o + qbase + (size_t)qrow * DIO;
+#pragma unroll
+      for (int db = 0; db < NDB; ++db) {
+        if (32 * db >= DIO) break;   // DIO is a multiple of 32
+#pragma unroll
+        for (int a = 0; a < 4; ++a) {
+          const u32x2 w = {pack_bf16x2(oacc[db][4 * a], oacc[db][4 * a + 1]),
+                           pack_bf16x2(oacc[db][4 * a + 2], oacc[db][4 * a + 3])};
+          *reinterpret_cast<u32x2*>(orow + 32 * db + 8 * a + 4 * grp) = w;
+        }
+      }
+    }
+    if constexpr (CHECK) {
+      act = sum_xor32(act);
+      absum = sum_xor32(absum);
+      const float c_tot = sum_xor32(aux[0] + aux[1]);
+      const float pred = c_tot * inv;
+      const float r = pred - act;
+      const float M = absum + __builtin_fabsf(pred);
+      // non-finite test on the bits (this file is built with relaxed NaN rules);
+      // a non-finite residual also fails the threshold comparison. An overflow
+      // of sum_j |O_ij| (a huge but finite row) would make the threshold
+      // infinite and pass any residual, so it counts as non-finite as well.
+      bool nonfinite = nonfinite_bits(r) || nonfinite_bits(absum);
+      uint8_t f = (__builtin_fabsf(r) <= p.tau_rel * M + p.tau_abs) ? 0 : 1;
+      // weighted check: pred_w = c_w / l against sum_j (-1)^j O_ij (the same
+      // threshold rule; |w_j| = 1 keeps M)
+      float pred_w = 0.f;
+      float sc_lhs = 0.f, sc_rhs = 0.f, sc_bound = 0.f;   // score check (debug outputs)
+      if constexpr (WCHK) {
+        act_w = sum_xor32(act_w);
+        pred_w = sum_xor32(auxw[0] + auxw[1]) * inv;
+        const float rw = pred_w - act_w;
+        nonfinite = nonfinite || nonfinite_bits(rw);
+        if (!(__builtin_fabsf(rw) <= p.tau_rel * (absum + __builtin_fabsf(pred_w)) + p.tau_abs)) f |= 4;
+      }
+      if constexpr (SCHK) {
+        // score check: sum over the full key tiles of s_ij against
+        // q_i . sum_k K_k over the same keys (the prefix of the K column sums
+        // up to the wave's first masked tile), within tau_s * |q_i| . sum_k |K_k|
+        int tw = Lk / BC;   // tiles without the key-range mask
+        if (CAUSAL) {
+          const int lim = wq_lo + off + 1;   // tiles wholly below the wave's diagonal
+          tw = min(tw, lim <= 0 ? 0 : lim / BC);
+        }
+        const size_t kro = ((size_t)bh * (p.ntk + 1) + tw) * D;
+        float rhs = 0.f, ms = 0.f;
+#pragma unroll
+        for (int s2 = 0; s2 < NDS; ++s2) {
+          const int c0 = 16 * s2 + 8 * grp;   // the lane's 8 columns of q
+          const f32x4 kp0 = *reinterpret_cast<const f32x4*>(p.kpre + kro + c0);
+          const f32x4 kp1 = *reinterpret_cast<const f32x4*>(p.kpre + kro + c0 + 4);
+          const f32x4 ka0 = *reinterpret_cast<const f32x4*>(p.kabs + kro + c0);
+          const f32x4 ka1 = *reinterpret_cast<const f32x4*>(p.kabs + kro + c0 + 4);
+          const float kp[8] = {kp0[0], kp0[1], kp0[2], kp0[3], kp1[0], kp1[1], kp1[2], kp1[3]};
+          const float ka[8] = {ka0[0], ka0[1], ka0[2], ka0[3], ka1[0], ka1[1], ka1[2], ka1[3]};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float qa = __uint_as_float(qf[s2][e] << 16);
+            const float qb = __uint_as_float(qf[s2][e] & 0xffff0000u);
+            rhs = __builtin_fmaf(qa, kp[2 * e], __builtin_fmaf(qb, kp[2 * e + 1], rhs));
+            ms = __builtin_fmaf(__builtin_fabsf(qa), ka[2 * e],
+                                __builtin_fmaf(__builtin_fabsf(qb), ka[2 * e + 1], ms));
+          }
+        }
+        // scores carry the softmax scale only in the exponent (exp2 of s * sl2):
+        // the sums compare raw q . k
+        const float lhs = sum_xor32(s_lhs);
+        rhs = sum_xor32(rhs);
+        ms = sum_xor32(ms);
+        const float rs = lhs - rhs;
+        nonfinite = nonfinite || nonfinite_bits(rs);
+        if (!(__builtin_fabsf(rs) <= p.tau_s * ms + p.tau_abs)) f |= 8;
+        sc_lhs = lhs;
+        sc_rhs = rhs;
+        sc_bound = ms;
+      }
+      if (nonfinite) f |= 3;
+      if (grp == 0 && qrow < Lq) {
+        const size_t ri = (size_t)bh * Lq + qrow;
+        p.resid[ri] = r;
+        p.flags[ri] = f;
+        if constexpr (INJECT) {
+          if (p.pred) p.pred[ri] = pred;
+          if (p.actual) p.actual[ri] = act;
+          if (p.pred_w) p.pred_w[ri] = pred_w;
+          if (p.actual_w) p.actual_w[ri] = WCHK ? act_w : 0.f;
+          if (p.s_lhs) p.s_lhs[ri] = sc_lhs;
+          if (p.s_rhs) p.s_rhs[ri] = sc_rhs;
+          if (p.s_bound) p.s_bound[ri] = sc_bound;
+        }
+      }
+    }
+
+    if (!has_next) break;
+    // on to the next item: its first tiles are in the ring (cont), else it
+    // starts like a first item
+    bh = nbh;
+    qt = nqt;
+    set_item();
+    primed = cont;
+    if (!cont) load_q(bh, qt);
   }
 }
 
+// ---- persistent launches: how many workgroups the device holds at once
+static std::atomic<bool> g_persist{true};
+void set_persistent(bool on) { g_persist.store(on); }
+bool get_persistent() { return g_persist.load(); }
+
+// Compute units of the stream's device (0 if unknown), cached per device.
+static int device_cus(hipStream_t stream) {
+  constexpr int kMaxDev = 64;
+  static std::atomic<int> cus[kMaxDev];
+  int dev = -1;
+  if (hipStreamGetDevice(stream, &dev) != hipSuccess || dev < 0 || dev >= kMaxDev) {
+    (void)hipGetLastError();
+    return 0;
+  }
+  int n = cus[dev].load();
+  if (n == 0) {
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    cus[dev].store(n);
+  }
+  return n;
+}
+
 template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false>
-static int launch_t(const FwdParams& p, hipStream_t stream) {
+static int launch_t(const FwdParams& p0, hipStream_t stream) {
+  FwdParams p = p0;
+  p.persist = 0;
+  if constexpr (!INJECT && !SPLIT && !SCHK && Cfg<D>::AHEAD >= 3) {
+    // one or two workgroups per CU (the occupancy the launch bounds give),
+    // a multiple of 8 so that workgroup b stays on XCD b mod 8; with the
+    // mask only for a head count divisible by 8 (the banded schedule)
+    const int per_cu = D == 64 ? 2 : 1;
+    const int g = (device_cus(stream) * per_cu) & ~7;
+    const int heads = p.n_items / p.n_qt;
+    if (g_persist.load() && g >= 8 && p.n_items > g && (!CAUSAL || (heads & 7) == 0)) {
+      p.persist = 1;
+      p.grid = g;
+    }
+  }
   // the thread's last-error slot may hold an error of an unrelated earlier
   // HIP call (made by the caller); clear it so that only this launch counts
   (void)hipGetLastError();
