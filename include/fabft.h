@@ -61,7 +61,8 @@ enum {
   FABFT_E_SCALE = -6,    /* scale negative, NaN or infinite */
   FABFT_E_FAULT = -7,    /* fault descriptor out of range */
   FABFT_E_THRESHOLD = -8, /* threshold negative or NaN */
-  FABFT_E_WORKSPACE = -9  /* workspace smaller than fabft_splitkv_workspace_bytes */
+  FABFT_E_WORKSPACE = -9, /* workspace smaller than fabft_splitkv_workspace_bytes */
+  FABFT_E_MODE = -10      /* a mode argument outside its documented values */
 };
 
 /* Detection flags, one byte per query row. */
@@ -239,19 +240,23 @@ void fabft_set_weighted_check(int on);
 int fabft_get_weighted_check(void);
 
 /*
- * Persistent workgroups (a launch shape, not part of the method; default:
- * on). With it on, fabft_attn_fwd and fabft_attn_fwd_nocheck launch only as
- * many workgroups as the device holds at once (one per compute unit, two at
- * d = 64) when there are more (head, query tile) items than that, each
- * workgroup running a fixed list of items; the next item's Q and first key
- * tiles load while the current item's last tiles and its epilogue run. It
- * applies without the mask, or with it when B * H is a multiple of 8, and
- * never to the split, debug, injection or score-check paths. Results are
- * bitwise the same either way (each row is computed by the same
- * instructions in the same order). 0 turns it off: one workgroup per item.
+ * Persistent workgroups (a launch shape, not part of the method). When on,
+ * fabft_attn_fwd and fabft_attn_fwd_nocheck launch only as many workgroups
+ * as the device holds at once (one per compute unit, two at d = 64) when
+ * there are more (head, query tile) items than that, each workgroup running
+ * a fixed list of items; the next item's Q and first key tiles load while
+ * the current item's last tiles and its epilogue run. It applies without the
+ * mask, or with it when B * H is a multiple of 8, and never to the split,
+ * debug, injection or score-check paths. Results are bitwise the same
+ * either way (each row is computed by the same instructions in the same
+ * order). Modes: FABFT_PERSIST_OFF (one workgroup per item),
+ * FABFT_PERSIST_AUTO (default: on for d = 96 and 128 when Lk <= 1024, where
+ * a workgroup's start-up is a large part of its work), FABFT_PERSIST_ALWAYS.
+ * fabft_set_persistent returns FABFT_E_MODE for any other value.
  * Process-global, not thread-safe.
  */
-void fabft_set_persistent(int on);
+enum { FABFT_PERSIST_OFF = 0, FABFT_PERSIST_AUTO = 1, FABFT_PERSIST_ALWAYS = 2 };
+int fabft_set_persistent(int mode);
 int fabft_get_persistent(void);
 
 /* Number of keys per key tile of the kernel for head dimension d (the unit

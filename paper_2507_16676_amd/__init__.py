@@ -28,8 +28,9 @@ _vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
 _fp = ctypes.POINTER(ctypes.c_float)
 
 FABFT_OK = 0
-E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE = \
-    -1, -2, -3, -4, -5, -6, -7, -8, -9
+E_NULL, E_SHAPE, E_HEADDIM, E_ALIGN, E_LAUNCH, E_SCALE, E_FAULT, E_THRESHOLD, E_WORKSPACE, \
+    E_MODE = -1, -2, -3, -4, -5, -6, -7, -8, -9, -10
+PERSIST_OFF, PERSIST_AUTO, PERSIST_ALWAYS = 0, 1, 2
 FLAG_RESID, FLAG_NONFINITE, FLAG_WEIGHTED, FLAG_SCORES = 1, 2, 4, 8
 SITE_NONE, SITE_S, SITE_P, SITE_O, SITE_V, SITE_C, SITE_L, SITE_M, SITE_Q, SITE_VS = range(10)
 SITES = {"none": SITE_NONE, "S": SITE_S, "P": SITE_P, "O": SITE_O, "V": SITE_V,
@@ -111,7 +112,7 @@ def _load() -> ctypes.CDLL:
     L.fabft_get_weighted_check.argtypes = []
     L.fabft_get_weighted_check.restype = _i
     L.fabft_set_persistent.argtypes = [_i]
-    L.fabft_set_persistent.restype = None
+    L.fabft_set_persistent.restype = _i
     L.fabft_get_persistent.argtypes = []
     L.fabft_get_persistent.restype = _i
     L.fabft_key_tile.argtypes = [_i]
@@ -206,14 +207,15 @@ def get_weighted_check() -> bool:
     return bool(_load().fabft_get_weighted_check())
 
 
-def set_persistent(on: bool):
-    """Persistent workgroups for attn_fwd (process-global, default on): a
-    launch shape only, the results are bitwise the same."""
-    _load().fabft_set_persistent(int(bool(on)))
+def set_persistent(mode: int):
+    """Persistent workgroups for attn_fwd (process-global): PERSIST_OFF,
+    PERSIST_AUTO (default) or PERSIST_ALWAYS. A launch shape only: the
+    results are bitwise the same."""
+    _check(_load().fabft_set_persistent(int(mode)), "fabft_set_persistent")
 
 
-def get_persistent() -> bool:
-    return bool(_load().fabft_get_persistent())
+def get_persistent() -> int:
+    return int(_load().fabft_get_persistent())
 
 
 def key_tile(d: int) -> int:
@@ -507,4 +509,5 @@ __all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_debug", "attn_fwd_splitkv", 
            "get_threshold", "set_weighted_check", "get_weighted_check", "set_persistent",
            "get_persistent", "key_tile",
            "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "MAX_FAULTS", "FLAG_RESID",
-           "FLAG_NONFINITE", "FLAG_WEIGHTED", "FLAG_SCORES"]
+           "FLAG_NONFINITE", "FLAG_WEIGHTED", "FLAG_SCORES", "PERSIST_OFF", "PERSIST_AUTO",
+           "PERSIST_ALWAYS"]

@@ -13,6 +13,9 @@
 #include "fabft_kernels.h"
 
 static_assert(FABFT_MAX_FAULTS == fabft::kMaxFaults, "fault list size");
+static_assert(FABFT_PERSIST_OFF == fabft::kPersistOff && FABFT_PERSIST_AUTO == fabft::kPersistAuto &&
+                  FABFT_PERSIST_ALWAYS == fabft::kPersistAlways,
+              "persistent modes");
 
 // Library-owned scratch of the allocation-free key split: one copy per GPU,
 // held from the library's load until the process ends. In host code the
@@ -442,9 +445,13 @@ float fabft_get_score_threshold(void) { return g_tau_s; }
 
 int fabft_get_weighted_check(void) { return g_wcheck; }
 
-void fabft_set_persistent(int on) { fabft::set_persistent(on != 0); }
+int fabft_set_persistent(int mode) {
+  if (mode < FABFT_PERSIST_OFF || mode > FABFT_PERSIST_ALWAYS) return FABFT_E_MODE;
+  fabft::set_persistent(mode);
+  return FABFT_OK;
+}
 
-int fabft_get_persistent(void) { return fabft::get_persistent() ? 1 : 0; }
+int fabft_get_persistent(void) { return fabft::get_persistent(); }
 
 int fabft_key_tile(int d) {
   if (!head_dim_ok(d)) return FABFT_E_HEADDIM;
@@ -468,6 +475,7 @@ const char* fabft_status_str(int status) {
     case FABFT_E_FAULT: return "fault descriptor out of range";
     case FABFT_E_THRESHOLD: return "threshold must be >= 0";
     case FABFT_E_WORKSPACE: return "workspace too small (see fabft_splitkv_workspace_bytes)";
+    case FABFT_E_MODE: return "mode argument out of range";
     default: return "unknown status";
   }
 }

@@ -66,12 +66,13 @@ struct FwdParams {
 
 // mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection,
 // 3: checksum on, one key split per workgroup (partial states to p.ws).
-// Modes 0 and 1 (without the score check) run as many workgroups as fit on
-// the device at once, each running a list of items, when there are more
-// items than that and set_persistent has not turned it off.
+// Modes 0 and 1 (without the score check) may run as many workgroups as fit
+// on the device at once, each running a list of items, when there are more
+// items than that (set_persistent: off, automatic, always).
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream);
-void set_persistent(bool on);
-bool get_persistent();
+enum { kPersistOff = 0, kPersistAuto = 1, kPersistAlways = 2 };
+void set_persistent(int mode);
+int get_persistent();
 int key_tile(int d);
 // Width the kernels compute with for a head dimension d (64, 96, 128 or
 // 256): d itself, or 128 for d = 96 (columns 96..127 are zero on chip).

@@ -1097,9 +1097,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
 }
 
 // ---- persistent launches: how many workgroups the device holds at once
-static std::atomic<bool> g_persist{true};
-void set_persistent(bool on) { g_persist.store(on); }
-bool get_persistent() { return g_persist.load(); }
+static std::atomic<int> g_persist{kPersistAuto};
+void set_persistent(int mode) { g_persist.store(mode); }
+int get_persistent() { return g_persist.load(); }
 
 // Compute units of the stream's device (0 if unknown), cached per device.
 static int device_cus(hipStream_t stream) {
@@ -1129,10 +1129,16 @@ static int launch_t(const FwdParams& p0, hipStream_t stream) {
     // one or two workgroups per CU (the occupancy the launch bounds give),
     // a multiple of 8 so that workgroup b stays on XCD b mod 8; with the
     // mask only for a head count divisible by 8 (the banded schedule)
+    // Automatic only for short rows at d = 96 and 128 (at most 16 key
+    // tiles), where a workgroup's start-up is a large part of its work;
+    // measured neutral at d = 64 and on long rows.
     const int per_cu = D == 64 ? 2 : 1;
     const int g = (device_cus(stream) * per_cu) & ~7;
     const int heads = p.n_items / p.n_qt;
-    if (g_persist.load() && g >= 8 && p.n_items > g && (!CAUSAL || (heads & 7) == 0)) {
+    const int mode = g_persist.load();
+    const bool want = mode == kPersistAlways ||
+                      (mode == kPersistAuto && D != 64 && (p.Lk + kBc - 1) / kBc <= 16);
+    if (want && g >= 8 && p.n_items > g && (!CAUSAL || (heads & 7) == 0)) {
       p.persist = 1;
       p.grid = g;
     }

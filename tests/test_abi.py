@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9):
+    for s in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9, -10):
         assert F.status_str(s) and F.status_str(s) != "unknown status"
     assert F.status_str(12345) == "unknown status"
 
@@ -278,3 +278,18 @@ def test_caller_tensor_checks():
         F._check_workspace(ws, "ws", 401, cpu)
     with pytest.raises(ValueError, match="contiguous"):
         F._check_workspace(torch.empty((10, 20))[:, ::2], "ws", 4, cpu)
+
+
+def test_persistent_mode_validation():
+    """The launch-shape switch takes off / automatic / always and refuses
+    anything else (no device work: the setting is host state)."""
+    L = F.lib()
+    assert L.fabft_get_persistent() == F.PERSIST_AUTO
+    for bad in (-1, 3, 99):
+        assert L.fabft_set_persistent(bad) == F.E_MODE
+        assert L.fabft_get_persistent() == F.PERSIST_AUTO
+    for m in (F.PERSIST_OFF, F.PERSIST_ALWAYS, F.PERSIST_AUTO):
+        assert L.fabft_set_persistent(m) == F.FABFT_OK and L.fabft_get_persistent() == m
+    with pytest.raises(F.FabftError):
+        F.set_persistent(5)
+    assert F.get_persistent() == F.PERSIST_AUTO

@@ -34,7 +34,7 @@ CASES = [
 
 
 def _run(q, k, v, causal, scale, persistent, check=True):
-    F.set_persistent(persistent)
+    F.set_persistent(F.PERSIST_ALWAYS if persistent else F.PERSIST_OFF)
     try:
         o = torch.full_like(q, float("nan"))
         if not check:
@@ -48,7 +48,7 @@ def _run(q, k, v, causal, scale, persistent, check=True):
         torch.cuda.synchronize()
         return o, r, f
     finally:
-        F.set_persistent(True)
+        F.set_persistent(F.PERSIST_AUTO)
 
 
 def _same(a, b):
@@ -66,7 +66,7 @@ def test_persistent_matches_one_item_per_workgroup(case):
     w = W.Workload(name, B, H, Lq, Lk, d, causal, d ** -0.5, seed=91)
     inp = W.make_inputs(w)
     q, k, v = G.dev_inputs(inp)
-    assert F.get_persistent()
+    assert F.get_persistent() == F.PERSIST_AUTO
     one = _run(q, k, v, causal, w.scale, False)
     per = _run(q, k, v, causal, w.scale, True)
     for a, b, what in zip(one, per, ("o", "resid", "flags")):
