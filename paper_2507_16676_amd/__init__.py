@@ -22,7 +22,10 @@ import os
 from dataclasses import dataclass
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libfabft.so")
+# the in-tree build, or another build of the same library named by FABFT_LIB
+# (the host-sanitized one of `python -m paper_2507_16676_amd.build
+# --host-sanitize OUT`)
+LIB_PATH = os.environ.get("FABFT_LIB") or os.path.join(_HERE, "libfabft.so")
 
 _vp, _i, _f = ctypes.c_void_p, ctypes.c_int, ctypes.c_float
 _fp = ctypes.POINTER(ctypes.c_float)

@@ -1,6 +1,15 @@
 """Build libfabft.so (HIP kernels for gfx950 + the C ABI) in-tree.
 
     python -m paper_2507_16676_amd.build [-v]
+    python -m paper_2507_16676_amd.build --host-sanitize OUT.so
+
+The second form builds a copy with AddressSanitizer and UndefinedBehavior-
+Sanitizer on the host code only (argument validation, launch set-up; the
+device code is built as usual) into OUT.so, leaving the in-tree library
+alone. Load it with FABFT_LIB=OUT.so and the ASan runtime preloaded, e.g.
+
+    ASAN_OPTIONS=detect_leaks=0 LD_PRELOAD=$(/opt/rocm/llvm/bin/clang -print-file-name=libclang_rt.asan-x86_64.so) \
+        FABFT_LIB=OUT.so python -m pytest tests/test_abi.py
 
 Compiles with hipcc for gfx950 only. Packed fp32 VALU instructions are
 switched off for device code (``-packed-fp32-ops``); the host pass warns that
@@ -60,6 +69,26 @@ def _run(cmd, verbose):
         print(msgs, flush=True)
 
 
+# every sanitizer flag is bound to the host pass (-Xarch_host): the device code
+# is built exactly as in the product library
+SANITIZERS = ("address", "undefined")
+HOST_SANITIZE = [f for s in SANITIZERS for f in ("-Xarch_host", "-fsanitize=" + s)] + [
+    "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
+
+
+def build_host_sanitized(out: str, verbose: bool = False) -> str:
+    """libfabft.so with ASan and UBSan on the host code, written to `out`."""
+    import tempfile
+    with tempfile.TemporaryDirectory(prefix="fabft_build_") as objdir:
+        cmds = build_cmds(out, objdir, HOST_SANITIZE)
+        link = cmds[-1]
+        cmds[-1] = (link[:-2] + [f for s in SANITIZERS for f in ("-Xarch_host", "-fsanitize=" + s)]
+                    + ["-shared-libsan"] + link[-2:])
+        for cmd in cmds:
+            _run(cmd, verbose)
+    return out
+
+
 def build(verbose: bool = False, extra=()) -> str:
     import tempfile
     tmp = LIB + f".tmp{os.getpid()}"
@@ -77,5 +106,8 @@ def build(verbose: bool = False, extra=()) -> str:
 
 if __name__ == "__main__":
     v = "-v" in sys.argv
+    if "--host-sanitize" in sys.argv:
+        print(build_host_sanitized(sys.argv[sys.argv.index("--host-sanitize") + 1], verbose=v))
+        sys.exit(0)
     extra = ["-Rpass-analysis=kernel-resource-usage"] if "--usage" in sys.argv else []
     print(build(verbose=v or bool(extra), extra=extra))
