@@ -177,9 +177,14 @@ void fabft_get_threshold(float* tau_rel, float* tau_abs);
  * workspace on the library stream: fabft_score_check_workspace_bytes(B, H,
  * Lk, d) bytes for a call, 16-byte aligned, caller-owned, kept in use (not
  * copied) while set; a call whose need exceeds it returns FABFT_E_WORKSPACE.
- * It also catches a fault in q_i that lands after the first key tile (the
- * right-hand side uses the final q_i for all full tiles); a score fault in
- * a masked tile, or a q fault present from the start, is not covered.
+ * The masked tiles of a row (the diagonal one, a ragged last one) have no
+ * such per-row prefix: there the kernel computes the tile's Q K^T a second
+ * time from the same operands and sets FABFT_FLAG_SCORES when the row's
+ * sums of its visible scores from the two products differ in any bit
+ * (a duplicated product, not a checksum). It also catches a fault in q_i
+ * that lands after the first key tile (the right-hand side uses the final
+ * q_i for all full tiles); a q fault present from the start changes both
+ * sides alike and is not covered.
  * d = 256 is not supported (FABFT_E_HEADDIM while the check is on).
  * workspace = NULL switches the check off. tau_s = 0 selects the default
  * (2^-22); a negative or NaN tau_s is FABFT_E_THRESHOLD. Process-global,

@@ -516,13 +516,25 @@ def score_check_fault(q, k, i: int, Lq: int, causal: bool, fault: FaultSpec,
     enters lhs if k lies in the full tiles; the right-hand side is unchanged.
     Q (row i, column j, from key tile t on): the scores of tiles >= t use the
     flipped q_ij, and rhs and the bound use it for every full tile (the q
-    the row holds at the end). Returns lhs, rhs, ms, n, flag (the score
-    flag: |lhs - rhs| > tau_s * ms + tau_abs with finite sums), nonfinite
-    (the sums are not finite: the row counts as non-finite instead), term
-    (the magnitude of the changed terms, sum of |x_j y_j| scaled by the flip,
-    which bounds what fp32 rounding of the kernel's scores can move) and
-    undetermined (a sum beyond 2^100: fp32 overflow inside the kernel's sums
-    decides the outcome)."""
+    the row holds at the end). Returns lhs, rhs, ms, n, row_flag (|lhs - rhs|
+    > tau_s * ms + tau_abs with finite sums), nonfinite (the sums are not
+    finite: the row counts as non-finite instead), term (the magnitude of
+    the changed terms, sum of |x_j y_j| scaled by the flip, which bounds what
+    fp32 rounding of the kernel's scores can move) and undetermined (a sum
+    beyond 2^100: fp32 overflow inside the kernel's sums decides the
+    outcome).
+
+    The keys past the full tiles that row i sees lie in masked tiles (the
+    diagonal one, a ragged last one), which have no per-row prefix of the K
+    sums; there the kernel sums the row's visible scores of each such tile
+    twice, from the product as stored and from a second product of the same
+    operands, and flags any difference. An S flip on such a key changes the
+    first sum by dsum = s' - s (a Q flip changes both products alike): the
+    two fp32 sums differ for certain when |dsum| exceeds their rounding
+    (2^-17 of A, the tile's sum of |s_ik| over the row's visible keys plus
+    |s'|), never when dsum = 0, and the outcome is left undetermined in
+    between; a non-finite s' always differs. Returned as dup_flag and
+    dup_undetermined; flag = row_flag or dup_flag."""
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
     r = score_check_row(q, k, i, Lq, causal, key_tile)
@@ -548,12 +560,34 @@ def score_check_fault(q, k, i: int, Lq: int, causal: bool, fault: FaultSpec,
             rhs = float(qn @ ks.sum(axis=0))
             ms = float(np.abs(qn) @ np.abs(ks).sum(axis=0))
             term = float(abs(qn[j] - q[i, j]) * np.abs(ks[:, j]).sum())
+    dup_flag = dup_und = False
+    Lk = k.shape[0]
+    last = min(Lk - 1, i + Lk - Lq) if causal else Lk - 1
+    if fault.row == i and fault.site == "S" and n <= fault.col <= last:
+        s = float(k[fault.col] @ q[i])
+        s32 = float(np.float32(s))
+        sn = flip_f32(s, fault.bit)
+        t0 = (fault.col // key_tile) * key_tile
+        keys = np.arange(t0, min(t0 + key_tile, last + 1))
+        a_sum = float(np.abs(k[keys] @ q[i]).sum())
+        if not np.isfinite(sn):
+            dup_flag = True
+        else:
+            dsum = sn - s32
+            a_sum += abs(sn)
+            if dsum == 0.0:
+                dup_flag = False
+            elif abs(dsum) > 2.0 ** -17 * a_sum:
+                dup_flag = True
+            else:
+                dup_und = True
     with np.errstate(invalid="ignore"):
         d = lhs - rhs
         nonfinite = bool(not np.isfinite(d) or not np.isfinite(ms))
-        flag = bool(not nonfinite and abs(d) > tau_s * ms + tau_abs)
+        row_flag = bool(not nonfinite and abs(d) > tau_s * ms + tau_abs)
         # sums near the fp32 range: whether the kernel's fp32 products and
         # sums overflow (and in which order) decides the outcome
         und = bool(not nonfinite and max(abs(lhs), abs(rhs), ms, term) > 2.0 ** 100)
-    return {"lhs": lhs, "rhs": rhs, "ms": ms, "n": n, "flag": flag, "nonfinite": nonfinite,
-            "term": term, "undetermined": und}
+    return {"lhs": lhs, "rhs": rhs, "ms": ms, "n": n, "row_flag": row_flag,
+            "dup_flag": dup_flag, "dup_undetermined": dup_und, "flag": row_flag or dup_flag,
+            "nonfinite": nonfinite, "term": term, "undetermined": und}

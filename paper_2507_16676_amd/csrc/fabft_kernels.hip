@@ -442,6 +442,9 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   // the end); with the weighted check, auxw [0] c_w hi, [1] c_w lo alike
   f32x4 aux, auxw;
   float s_lhs;    // score check: sum of this lane's scores in full tiles
+  // score check on masked tiles (the diagonal and ragged ones): this lane's
+  // sum of its visible scores, and the same sum from a second Q K^T product
+  float d_lhs, d_rhs;
   float m2_run;   // running max, exp2 domain (s * scale * log2 e)
   const float sl2 = p.sl2;
 
@@ -651,8 +654,11 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb)
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          if (32 * kb + 16 * (i >> 3) + (i & 7) > rel) sacc[kb][i] = -__builtin_inff();
+        for (int i = 0; i < 16; ++i) {
+          const bool hidden = 32 * kb + 16 * (i >> 3) + (i & 7) > rel;
+          if constexpr (SCHK) d_lhs += hidden ? 0.f : sacc[kb][i];
+          if (hidden) sacc[kb][i] = -__builtin_inff();
+        }
     }
     // one chain of three-input maxima (v_max3): one instruction per two scores
     float mx = __builtin_fmaxf(sacc[0][0], sacc[0][1]);
@@ -808,6 +814,31 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
         }
       }
     }
+    if constexpr (SCHK) {
+      // a masked tile has no per-row prefix of the K column sums, so its
+      // scores are checked by a second Q K^T product (same operands and
+      // instructions, summed over the same visible keys; the two sums agree
+      // bit for bit unless a stored score changed). The accumulators start
+      // from an opaque zero, so that the compiler keeps the second product.
+      if (need_mask) {
+        f32x16 r[NKB];
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb) {
+          r[kb] = f32x16{};
+          asm volatile("" : "+v"(r[kb]));
+        }
+#pragma unroll
+        for (int i = 0; i < NQK; ++i) r[i % NKB] = mfma32(kread(i), qf[i / NKB], r[i % NKB]);
+        int lim = Lk - 1;
+        if (CAUSAL) lim = min(lim, qrow + off);
+        const int rel = lim - (kv0 + 8 * grp);
+#pragma unroll
+        for (int kb = 0; kb < NKB; ++kb)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            d_rhs += (32 * kb + 16 * (i >> 3) + (i & 7) > rel) ? 0.f : r[kb][i];
+      }
+    }
   };
 
   // ---- pipeline: AHEAD tiles loading while tile t is processed
@@ -864,6 +895,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     aux = f32x4{};
     auxw = f32x4{};
     s_lhs = 0.f;
+    d_lhs = 0.f;
+    d_rhs = 0.f;
     m2_run = -__builtin_inff();
     if (!primed && t_end > t_lo) {
       // after a previous item whose ring drained, every wave must be done with
@@ -1064,6 +1097,8 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
         const float rs = lhs - rhs;
         nonfinite = nonfinite || nonfinite_bits(rs);
         if (!(__builtin_fabsf(rs) <= p.tau_s * ms + p.tau_abs)) f |= 8;
+        // masked tiles: the two products' sums must agree bit for bit
+        if (opaque_bits(sum_xor32(d_lhs)) != opaque_bits(sum_xor32(d_rhs))) f |= 8;
         sc_lhs = lhs;
         sc_rhs = rhs;
         sc_bound = ms;

@@ -443,4 +443,39 @@ def test_score_check_fault_brute_force(site, bit):
         assert math.isclose(pr["ms"], ms, rel_tol=1e-12)
         assert pr["nonfinite"] == (not math.isfinite(lhs - rhs) or not math.isfinite(ms))
         if not pr["nonfinite"]:
-            assert pr["flag"] == (abs(lhs - rhs) > 2.0 ** -22 * ms)
+            assert pr["row_flag"] == (abs(lhs - rhs) > 2.0 ** -22 * ms)
+            assert not pr["dup_flag"] and pr["flag"] == pr["row_flag"]
+
+
+@pytest.mark.parametrize("bit", [0, 5, 12, 20, 23, 24, 27, 29, 30, 31])
+def test_masked_tile_duplicate_check_brute_force(bit):
+    """An S flip on a key past the full tiles (the diagonal tile here): the
+    row check does not see it, the duplicate product does. Brute force: the
+    tile's visible scores summed in fp32 with the flipped value against the
+    same sum without it (in two lane halves, as the kernel adds them); the
+    prediction, where it is not left open, must match (causal 150 x 150)."""
+    Lq = Lk = 150
+    q, k, _ = _inputs(Lq, Lk, 3, seed=91)
+    for i in (70, 100, 149):
+        r0 = FM.score_check_row(q, k, i, Lq, True)
+        t0 = (i // 64) * 64
+        assert r0["n"] <= t0
+        for col in sorted({t0, (t0 + i) // 2, i}):
+            pr = FM.score_check_fault(q, k, i, Lq, True, FM.FaultSpec("S", i, col, 0, bit))
+            assert pr["lhs"] == r0["lhs"] and pr["rhs"] == r0["rhs"] and not pr["row_flag"]
+            def tile_sum(flip):
+                halves = [np.float32(0.0), np.float32(0.0)]
+                for kk in range(t0, i + 1):
+                    sc = f32(sum(float(q[i][j]) * float(k[kk][j]) for j in range(3)))
+                    if flip and kk == col:
+                        sc = f32_flip(sc, bit)
+                    h = ((kk - t0) >> 3) & 1
+                    with np.errstate(over="ignore", invalid="ignore"):
+                        halves[h] = np.float32(halves[h] + np.float32(sc))
+                with np.errstate(over="ignore", invalid="ignore"):
+                    return np.float32(halves[0] + halves[1])
+            a, b = tile_sum(True), tile_sum(False)
+            differ = a.tobytes() != b.tobytes()
+            if not pr["dup_undetermined"]:
+                assert pr["dup_flag"] == differ, (i, col, bit, a, b)
+                assert pr["flag"] == pr["dup_flag"]

@@ -68,14 +68,19 @@ def test_score_faults_in_full_tiles_are_flagged(score_check):
     assert caught_off == 0
 
 
-def test_not_covered_q_and_diagonal(score_check):
+def test_q_faults_and_the_masked_tiles(score_check):
     w = CASES[0]
     q, k, v = G.dev_inputs(W.make_inputs(w))
-    # the score of key 250 for row 250 sits in the masked diagonal tile
-    f = F.Fault("S", b=0, h=0, row=250, col=250, bit=24)
-    o, r, fl, _, _ = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale, fault=f)
-    torch.cuda.synchronize()
-    assert (int(fl[0, 0, 250]) & F.FLAG_SCORES) == 0
+    # the score of key 250 for row 250 sits in the masked diagonal tile: the
+    # second product of that tile catches it, and only that row is flagged
+    for col, bit in ((250, 24), (200, 29), (192, 30)):
+        f = F.Fault("S", b=0, h=0, row=250, col=col, bit=bit)
+        o, r, fl, _, _ = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale, fault=f)
+        torch.cuda.synchronize()
+        assert int(fl[0, 0, 250]) & F.FLAG_SCORES, (col, bit)
+        others = fl.clone()
+        others[0, 0, 250] = 0
+        assert int(others.sum()) == 0
     # a q register fault present from the first tile on changes both sides
     # of the score check alike ...
     f = F.Fault("Q", b=0, h=0, row=250, col=3, tile=0, bit=10)
@@ -212,7 +217,7 @@ def test_score_faults_match_the_oracle(w, score_check):
         assert abs(gr - pr["rhs"]) <= tol, (f, gr, pr)
         assert abs(gb - pr["ms"]) <= tol, (f, gb, pr)
         ratio = abs(pr["lhs"] - pr["rhs"]) / (tau_s * pr["ms"]) if pr["ms"] > 0 else 0.0
-        if 0.5 <= ratio <= 2.0:
+        if pr["dup_undetermined"] or (0.5 <= ratio <= 2.0 and not pr["dup_flag"]):
             continue
         n_dec += 1
         agree += bool(fl & F.FLAG_SCORES) == pr["flag"]
