@@ -31,9 +31,10 @@
 //  * The K rows feeding MFMA row r are permuted (bits 2 and 3 of r swapped)
 //    so that the S^T accumulator of a lane already holds, for each 16-key
 //    step of P V, the 8 consecutive keys its B operand needs.
-//  * sumrow(V) of a key tile is computed from LDS by the whole workgroup
-//    (8 threads per key, 4 at d = 256; fp32 via v_dot2 and a DPP reduction)
-//    while the tile before it is processed, and stored as a bf16 pair
+//  * sumrow(V) of a key tile is computed from LDS by the workgroup (four
+//    threads per key; at d = 128 on waves 0-3 only, one per SIMD; fp32 via
+//    v_dot2 and a DPP reduction) while the tile before it is processed,
+//    and stored as a bf16 pair
 //    hi + lo (hi = bf16(vs), lo = bf16(vs - hi); |vs - hi - lo| <=
 //    2^-17|vs|) in an 8-row operand [sumrow hi; sumrow lo; ones; 0; weighted
 //    hi; weighted lo; 0; 0]: one sum per key and tile shared by all query rows
@@ -54,6 +55,10 @@
 //    registers; c and l come out the same either way.
 //  * Masking (causal diagonal tiles, the ragged last tile) sets a score to
 //    -inf, whose exponential is exactly 0.
+//  * Persistent launch (optional): one or two workgroups per CU each run a
+//    list of (head, query tile) items; when an item has a multiple of four
+//    key tiles, the next item's first tiles load into the ring during its
+//    last steps and its Q during the epilogue.
 //  * Lazy rescaling: the running max used for the exponentials is moved only
 //    when a tile's max exceeds it by more than 8 in the exp2 domain, so
 //    p <= 256 and o, l, c are rescaled (alpha != 1) rarely; o*alpha is
@@ -700,7 +705,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     }
 
     // c = c*alpha + sumrow(V) p~ and l = l*alpha + sum p~ (Alg. 3): the
-    // c / l MFMA reads p~ before the P site and the P V product
+    // c / l products read p~ before the P site and the P V product
     if (__ballot(alpha != 1.f)) {
 #pragma unroll
       for (int db = 0; db < NDB; ++db)
