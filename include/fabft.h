@@ -99,6 +99,24 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v,
                            int causal, float scale);
 
 /*
+ * The checksum hosted by Algorithm 1 instead of Algorithm 3 (Section III-B:
+ * the per-query check of Eq. 8 needs only the exponentials and their sum, so
+ * either algorithm can carry it). A first pass over the keys takes each
+ * row's maximum score m_N (K only); a second pass accumulates o, l and
+ * c = sum_k e^{s_k - m_N} sumrow_k(V) with that fixed maximum (no rescaling),
+ * then O = o / l, pred = c / l and the check as in fabft_attn_fwd. Same
+ * arguments, outputs, layouts, threshold and weighted check; O agrees with
+ * fabft_attn_fwd to rounding (the exponentials use another reference
+ * maximum), not bit for bit. Costs the Q K^T product twice. Returns
+ * FABFT_E_MODE while the score check (fabft_set_score_check) is on: that
+ * check runs in the one-pass kernels only.
+ */
+int fabft_attn_fwd_twopass(const void* q, const void* k, const void* v,
+                           void* o, float* resid, uint8_t* flags,
+                           int B, int H, int Lq, int Lk, int d, int causal,
+                           float scale);
+
+/*
  * Bytes of workspace that fabft_attn_fwd_splitkv needs: one partial-state
  * record of (w + 4) floats per (b, h, query row, split), w the compute width
  * (d, or 128 for d = 96). Negative status for d not 64, 96, 128 or 256, a size

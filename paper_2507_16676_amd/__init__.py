@@ -73,6 +73,8 @@ def _load() -> ctypes.CDLL:
     L.fabft_attn_fwd.restype = _i
     L.fabft_attn_fwd_nocheck.argtypes = [_vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f]
     L.fabft_attn_fwd_nocheck.restype = _i
+    L.fabft_attn_fwd_twopass.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f]
+    L.fabft_attn_fwd_twopass.restype = _i
     L.fabft_attn_fwd_inject.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                         _f, ctypes.POINTER(FabftFault), _vp, _vp, _vp, _vp]
     L.fabft_attn_fwd_inject.restype = _i
@@ -128,7 +130,8 @@ def _load() -> ctypes.CDLL:
     return L
 
 
-EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_inject",
+EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_twopass",
+           "fabft_attn_fwd_inject",
            "fabft_attn_fwd_inject_n", "fabft_attn_fwd_debug", "fabft_score_check_workspace_bytes",
            "fabft_set_score_check", "fabft_get_score_threshold",
            "fabft_attn_fwd_splitkv", "fabft_splitkv_workspace_bytes",
@@ -314,6 +317,32 @@ def attn_fwd(q, k, v, causal: bool = False, scale: float | None = None, check: b
     _check(_load().fabft_attn_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
                                resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
                                int(bool(causal)), scale), "fabft_attn_fwd")
+    return o, resid, flags
+
+
+def attn_fwd_twopass(q, k, v, causal: bool = False, scale: float | None = None, out=None):
+    """Flash-ABFT checksum on Algorithm 1 (the row max in a first pass over
+    the keys, then o, l and c with that fixed max). Returns (o, resid, flags)
+    with the meaning of attn_fwd's. out: optional preallocated (o, resid,
+    flags)."""
+    import torch
+    B, H, Lq, Lk, d = _shape(q, k, v)
+    scale = 1.0 / math.sqrt(d) if scale is None else float(scale)
+    dev = q.device
+    if out is not None:
+        if len(out) != 3:
+            raise ValueError("out must be (o, resid, flags)")
+        o = _check_out(out[0], "out[0] (o)", q.shape, torch.bfloat16, dev)
+        resid = _check_out(out[1], "out[1] (resid)", (B, H, Lq), torch.float32, dev)
+        flags = _check_out(out[2], "out[2] (flags)", (B, H, Lq), torch.uint8, dev)
+    else:
+        o = torch.empty_like(q)
+        resid = torch.empty((B, H, Lq), dtype=torch.float32, device=dev)
+        flags = torch.empty((B, H, Lq), dtype=torch.uint8, device=dev)
+    _stream(dev)
+    _check(_load().fabft_attn_fwd_twopass(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                       resid.data_ptr(), flags.data_ptr(), B, H, Lq, Lk, d,
+                                       int(bool(causal)), scale), "fabft_attn_fwd_twopass")
     return o, resid, flags
 
 
@@ -505,7 +534,7 @@ def attn_fwd_inject(q, k, v, causal: bool = False, scale: float | None = None,
     return o, resid, flags, pred, actual
 
 
-__all__ = ["attn_fwd", "attn_fwd_inject", "attn_fwd_debug", "attn_fwd_splitkv", "splitkv_workspace_bytes",
+__all__ = ["attn_fwd", "attn_fwd_twopass", "attn_fwd_inject", "attn_fwd_debug", "attn_fwd_splitkv", "splitkv_workspace_bytes",
            "splitkv_default_splits",
            "global_check", "recompute_flagged", "Fault", "FabftError", "set_threshold",
            "set_score_check", "score_check_workspace_bytes", "get_score_threshold",

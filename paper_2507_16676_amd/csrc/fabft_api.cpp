@@ -161,6 +161,19 @@ int fabft_attn_fwd_nocheck(const void* q, const void* k, const void* v, void* o,
                 causal, 0, B * H);
 }
 
+int fabft_attn_fwd_twopass(const void* q, const void* k, const void* v, void* o, float* resid,
+                           uint8_t* flags, int B, int H, int Lq, int Lk, int d, int causal,
+                           float scale) {
+  int n_qt = 0, grid = 0;
+  int rc = validate(q, k, v, o, B, H, Lq, Lk, d, scale, &n_qt, &grid);
+  if (rc != FABFT_OK) return rc;
+  if (!resid || !flags) return FABFT_E_NULL;
+  // the score check runs in the one-pass kernels only
+  if (g_sws) return FABFT_E_MODE;
+  return launch(make_params(q, k, v, o, resid, flags, Lq, Lk, d, scale, n_qt, grid), d, causal, 4,
+                B * H);
+}
+
 }  // extern "C"
 
 namespace {

@@ -338,7 +338,8 @@ struct StageId {
 // WCHK: the weighted second checksum is compiled in (only with CHECK).
 // SPLIT: the workgroup runs one key split and writes partial row states.
 // SCHK: the score check is compiled in (only with CHECK, not with SPLIT).
-template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false>
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false,
+          bool TWOPASS = false>
 __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(FwdParams p) {
   constexpr int kWaves = Cfg<D>::WAVES;
   constexpr int kThreads = Cfg<D>::THREADS;
@@ -355,7 +356,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   // a workgroup may run a list of items (p.persist), handing the LDS ring
   // from one item to the next: the next item's Q and first key tiles load
   // while the current item's last tiles and epilogue run
-  constexpr bool kPersist = !INJECT && !SPLIT && !SCHK && Cfg<D>::AHEAD >= 3;
+  constexpr bool kPersist = !INJECT && !SPLIT && !SCHK && !TWOPASS && Cfg<D>::AHEAD >= 3;
 
   __shared__ __attribute__((aligned(16))) Ring<D> ring;
 
@@ -451,6 +452,12 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   // sum of its visible scores, and the same sum from a second Q K^T product
   float d_lhs, d_rhs;
   float m2_run;   // running max, exp2 domain (s * scale * log2 e)
+  // Algorithm 1 (TWOPASS): pass 0 streams K only and takes each row's max
+  // over all its keys (m_acc, score units); pass 1 is the loop below with the
+  // running max fixed at that value, so no rescale ever happens (alpha = 1).
+  // One-pass kernels run pass 1 only.
+  int pass = 1;
+  float m_acc = -__builtin_inff();
   const float sl2 = p.sl2;
 
   // constant rows of the c / l operand in every stage (visible after the
@@ -511,7 +518,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
       constexpr uint32_t kOff = offsetof(Ring<D>, k) + S * sizeof(Ring<D>::k[0]);
       constexpr uint32_t vOff = offsetof(Ring<D>, v) + S * sizeof(Ring<D>::v[0]);
       buffer_load_lds16(kr, kvo[j], soff, wl + kOff + j * kThreads * 16);
-      buffer_load_lds16(vr, vvo[j], soff, wl + vOff + j * kThreads * 16);
+      if (!TWOPASS || pass != 0) buffer_load_lds16(vr, vvo[j], soff, wl + vOff + j * kThreads * 16);
     }
   };
 
@@ -673,6 +680,12 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
       for (int i = (kb == 0 ? 2 : 0); i < 16; i += 2)
         mx = __builtin_fmaxf(__builtin_fmaxf(mx, sacc[kb][i]), sacc[kb][i + 1]);
     mx = max_xor32(mx);
+    if constexpr (TWOPASS) {
+      if (pass == 0) {
+        m_acc = __builtin_fmaxf(m_acc, mx);
+        return;
+      }
+    }
     // lazy running max in the exp2 domain
     const float mt2 = (mx == -__builtin_inff()) ? -__builtin_inff() : mx * sl2;
     const float m2_new = (mt2 > m2_run + kLazy) ? mt2 : m2_run;
@@ -850,6 +863,24 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   constexpr int LPT = 2 * NLD;   // loads per thread per tile (K and V)
   // wait until at most n (0 .. AHEAD-1) tiles of this wave's loads are in flight
   auto wait_tiles = [&](int n) __attribute__((always_inline)) {
+    if constexpr (TWOPASS) {
+      if (pass == 0) {   // K loads only: NLD per tile
+        if constexpr (AHEAD >= 3) {
+          if (n >= 2) {
+            wait_vmcnt<2 * NLD>();
+            return;
+          }
+        }
+        if constexpr (AHEAD >= 2) {
+          if (n == 1) {
+            wait_vmcnt<NLD>();
+            return;
+          }
+        }
+        wait_vmcnt<0>();
+        return;
+      }
+    }
     if constexpr (AHEAD >= 3) {
       if (n >= 2) {
         wait_vmcnt<2 * LPT>();
@@ -903,88 +934,99 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     d_lhs = 0.f;
     d_rhs = 0.f;
     m2_run = -__builtin_inff();
-    if (!primed && t_end > t_lo) {
-      // after a previous item whose ring drained, every wave must be done with
-      // its stages before they take new tiles
-      if (kPersist && k > 0) __syncthreads();
-      issue(StageId<0>(), t_lo);
-      if constexpr (AHEAD >= 2) issue(StageId<1>(), t_lo + 1);
-      if constexpr (AHEAD >= 3) {
-        issue(StageId<2>(), t_lo + 2);
-        // first tile complete; the next two may be outstanding
-        wait_tiles(min(2, t_end - 1 - t_lo));
-        __syncthreads();
-        if constexpr (CHECK) sumrow(StageId<0>());
-      }
-    }
-    // A use of Q here, on every path into the loop, puts the compiler's own
-    // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
-    // also waits for the first tiles) before the loop rather than inside it.
+    m_acc = -__builtin_inff();
+    // (unrolled: each pass is compiled with its own constant pass number)
 #pragma unroll
-    for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
-    static_assert(kStages == 4 || kStages == 2, "the loop below is unrolled over the stages");
-    static_assert(AHEAD == kStages - 1, "the stage of tile t-1 takes tile t+AHEAD");
-    auto step = [&](auto S_, int t) __attribute__((always_inline)) {
-      constexpr int S = decltype(S_)::value;
-      if constexpr (AHEAD >= 3) {
-        // tile t+1 complete (tile t+2 may still be in flight); after the
-        // barrier every wave is done with tile t-1, whose stage takes tile t+3
-        wait_tiles(min(1, te_v - 2 - t));
-        __syncthreads();
-      } else {
-        // tile t complete; after the barrier every wave is done with tile t-1,
-        // whose stage takes tile t+1, loading while tile t is processed
-        wait_tiles(0);
-        __syncthreads();
-        issue(StageId<(S + 1) % kStages>(), t + 1);
-        if constexpr (CHECK) {
-          sumrow(S_);
+    for (pass = TWOPASS ? 0 : 1; pass < 2; ++pass) {
+      if (TWOPASS && pass == 1) m2_run = (m_acc == -__builtin_inff()) ? m_acc : m_acc * sl2;
+      if (!primed && t_end > t_lo) {
+        // after a previous item whose ring drained (or the first pass of
+        // Algorithm 1), every wave must be done with its stages before they
+        // take new tiles
+        if ((kPersist && k > 0) || (TWOPASS && pass == 1)) __syncthreads();
+        issue(StageId<0>(), t_lo);
+        if constexpr (AHEAD >= 2) issue(StageId<1>(), t_lo + 1);
+        if constexpr (AHEAD >= 3) {
+          issue(StageId<2>(), t_lo + 2);
+          // first tile complete; the next two may be outstanding
+          wait_tiles(min(2, t_end - 1 - t_lo));
           __syncthreads();
+          if constexpr (CHECK) {
+            if (pass == 1) sumrow(StageId<0>());
+          }
         }
       }
-      if constexpr (INJECT) {
-        // V site: flip a bit of V[row][col] in this workgroup's copy of the
-        // tile, after its sumrow was taken and before any wave reads it; VS
-        // site (checker state): the same for the tile's sumrow operand (col 0:
-        // hi part, col 1: lo part). The condition is uniform over the
-        // workgroup; faults apply one after another.
-        bool hit = false;
-        for (int fi = 0; fi < p.nf; ++fi) {
-          const FaultDesc fd = p.f[fi];
-          if ((fd.site == 4 || fd.site == 9) && bh == fd.bh && qt == fd.tile) {
-            const int key = fd.row - t * BC;
-            if (key >= 0 && key < BC) {
-              hit = true;
-              if (tid == 0) {
-                uint16_t* e = fd.site == 4
-                                  ? ring.v[S] + Tile<D>::vidx(key, fd.col >> 3) + (fd.col & 7)
-                                  : &ring.vsm[S][kRowVsHi + fd.col][key];
-                *e = (uint16_t)(*e ^ (1u << fd.bit));
-              }
+      // A use of Q here, on every path into the loop, puts the compiler's own
+      // wait for the Q loads (vmcnt(0): it does not count the tile loads, so it
+      // also waits for the first tiles) before the loop rather than inside it.
+#pragma unroll
+      for (int s = 0; s < NDS; ++s) asm volatile("" : : "v"(qf[s]));
+      static_assert(kStages == 4 || kStages == 2, "the loop below is unrolled over the stages");
+      static_assert(AHEAD == kStages - 1, "the stage of tile t-1 takes tile t+AHEAD");
+      auto step = [&](auto S_, int t) __attribute__((always_inline)) {
+        constexpr int S = decltype(S_)::value;
+        if constexpr (AHEAD >= 3) {
+          // tile t+1 complete (tile t+2 may still be in flight); after the
+          // barrier every wave is done with tile t-1, whose stage takes tile t+3
+          wait_tiles(min(1, te_v - 2 - t));
+          __syncthreads();
+        } else {
+          // tile t complete; after the barrier every wave is done with tile t-1,
+          // whose stage takes tile t+1, loading while tile t is processed
+          wait_tiles(0);
+          __syncthreads();
+          issue(StageId<(S + 1) % kStages>(), t + 1);
+          if constexpr (CHECK) {
+            if (pass == 1) {
+              sumrow(S_);
+              __syncthreads();
             }
           }
         }
-        if (hit) __syncthreads();
-      }
-      // waves whose rows see none of this tile's keys, or that hold no row
-      // below Lq, skip it (they still load and take sumrow for the others)
-      if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(S_, t);
-      if constexpr (AHEAD >= 3) {
-        issue(StageId<(S + 3) % kStages>(), t + 3);
-        if constexpr (CHECK) {
-          if (t + 1 < te_v) sumrow(StageId<(S + 1) % kStages>());
+        if constexpr (INJECT) {
+          // V site: flip a bit of V[row][col] in this workgroup's copy of the
+          // tile, after its sumrow was taken and before any wave reads it; VS
+          // site (checker state): the same for the tile's sumrow operand (col 0:
+          // hi part, col 1: lo part). The condition is uniform over the
+          // workgroup; faults apply one after another.
+          bool hit = false;
+          for (int fi = 0; fi < p.nf; ++fi) {
+            const FaultDesc fd = p.f[fi];
+            if ((fd.site == 4 || fd.site == 9) && bh == fd.bh && qt == fd.tile) {
+              const int key = fd.row - t * BC;
+              if (key >= 0 && key < BC) {
+                hit = true;
+                if (tid == 0) {
+                  uint16_t* e = fd.site == 4
+                                    ? ring.v[S] + Tile<D>::vidx(key, fd.col >> 3) + (fd.col & 7)
+                                    : &ring.vsm[S][kRowVsHi + fd.col][key];
+                  *e = (uint16_t)(*e ^ (1u << fd.bit));
+                }
+              }
+            }
+          }
+          if (hit) __syncthreads();
         }
-      }
-    };
-    for (int t = t_lo; t < t_end; t += kStages) {
-      step(StageId<0>(), t);
-      if (t + 1 >= t_end) break;
-      step(StageId<1>(), t + 1);
-      if constexpr (kStages == 4) {
-        if (t + 2 >= t_end) break;
-        step(StageId<2 % kStages>(), t + 2);
-        if (t + 3 >= t_end) break;
-        step(StageId<3 % kStages>(), t + 3);
+        // waves whose rows see none of this tile's keys, or that hold no row
+        // below Lq, skip it (they still load and take sumrow for the others)
+        if (wq_lo < Lq && (!CAUSAL || t * BC <= wq_lo + 31 + off)) compute(S_, t);
+        if constexpr (AHEAD >= 3) {
+          issue(StageId<(S + 3) % kStages>(), t + 3);
+          if constexpr (CHECK) {
+            if (t + 1 < te_v && pass == 1) sumrow(StageId<(S + 1) % kStages>());
+          }
+        }
+      };
+      for (int t = t_lo; t < t_end; t += kStages) {
+        step(StageId<0>(), t);
+        if (t + 1 >= t_end) break;
+        step(StageId<1>(), t + 1);
+        if constexpr (kStages == 4) {
+          if (t + 2 >= t_end) break;
+          step(StageId<2 % kStages>(), t + 2);
+          if (t + 3 >= t_end) break;
+          step(StageId<3 % kStages>(), t + 3);
+        }
       }
     }
     // the next item's Q loads while this item's epilogue runs (q is not read
@@ -1161,11 +1203,12 @@ static int device_cus(hipStream_t stream) {
   return n;
 }
 
-template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false>
+template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false,
+          bool TWOPASS = false>
 static int launch_t(const FwdParams& p0, hipStream_t stream) {
   FwdParams p = p0;
   p.persist = 0;
-  if constexpr (!INJECT && !SPLIT && !SCHK && Cfg<D>::AHEAD >= 3) {
+  if constexpr (!INJECT && !SPLIT && !SCHK && !TWOPASS && Cfg<D>::AHEAD >= 3) {
     // one or two workgroups per CU (the occupancy the launch bounds give),
     // a multiple of 8 so that workgroup b stays on XCD b mod 8; with the
     // mask only for a head count divisible by 8 (the banded schedule)
@@ -1186,7 +1229,7 @@ static int launch_t(const FwdParams& p0, hipStream_t stream) {
   // the thread's last-error slot may hold an error of an unrelated earlier
   // HIP call (made by the caller); clear it so that only this launch counts
   (void)hipGetLastError();
-  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK, SPLIT, SCHK>), dim3(p.grid),
+  hipLaunchKernelGGL((fwd_kernel<D, CAUSAL, CHECK, INJECT, WCHK, SPLIT, SCHK, TWOPASS>), dim3(p.grid),
                      dim3(Cfg<D>::THREADS), 0, stream, p);
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
@@ -1194,8 +1237,12 @@ static int launch_t(const FwdParams& p0, hipStream_t stream) {
 template <int D, bool CAUSAL>
 static int launch_c(const FwdParams& p, int mode, hipStream_t s) {
   // mode 0: no checksum, 1: checksum, 2: checksum + injection/debug,
-  // 3: checksum, key split
+  // 3: checksum, key split, 4: checksum, two passes (Algorithm 1)
   if (mode == 0) return launch_t<D, CAUSAL, false, false, false, false>(p, s);
+  if (mode == 4) {
+    if (p.wcheck) return launch_t<D, CAUSAL, true, false, true, false, false, true>(p, s);
+    return launch_t<D, CAUSAL, true, false, false, false, false, true>(p, s);
+  }
   if constexpr (D != 256) {
     // the score check (not built for the one-wave-per-SIMD width 256)
     if (p.kpre && (mode == 1 || mode == 2)) {

@@ -87,6 +87,31 @@ def test_fwd_rejects_bad_arguments(args, code):
     assert F.lib().fabft_attn_fwd(*args) == code
 
 
+@pytest.mark.parametrize("args,code", [
+    ((0, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
+    ((P, P, P, P, 0, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
+    ((P, P, P, P, P, 0, 1, 1, 8, 8, 128, 0, 1.0), F.E_NULL),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 80, 0, 1.0), F.E_HEADDIM),
+    ((P, P, P, P, P, P, 1, 1, 0, 8, 128, 0, 1.0), F.E_SHAPE),
+    ((P, P, P, P, P, P, 1, 1, 1, 8388544, 128, 0, 1.0), F.E_SHAPE),
+    ((P + 2, P, P, P, P, P, 1, 1, 8, 8, 128, 0, 1.0), F.E_ALIGN),
+    ((P, P, P, P, P, P, 1, 1, 8, 8, 128, 0, -0.5), F.E_SCALE),
+])
+def test_twopass_rejects_bad_arguments(args, code):
+    assert F.lib().fabft_attn_fwd_twopass(*args) == code
+
+
+def test_twopass_rejects_the_score_check():
+    """The score check runs in the one-pass kernels only: with it on, the
+    two-pass entry point refuses the call before any launch."""
+    L = F.lib()
+    try:
+        assert L.fabft_set_score_check(P, 1 << 20, 0.0) == F.FABFT_OK
+        assert L.fabft_attn_fwd_twopass(P, P, P, P, P, P, 1, 2, 8, 8, 128, 1, 0.1) == F.E_MODE
+    finally:
+        assert L.fabft_set_score_check(None, 0, 0.0) == F.FABFT_OK
+
+
 def test_nocheck_rejects_bad_arguments():
     lib = F.lib()
     assert lib.fabft_attn_fwd_nocheck(P, P, P, 0, 1, 1, 8, 8, 128, 0, 1.0) == F.E_NULL
