@@ -305,6 +305,9 @@ def main():
                     help="also run the weighted second checksum (an extension)")
     ap.add_argument("--score-check", action="store_true",
                     help="also run the score check (an extension; its K-sum pre-pass is timed)")
+    ap.add_argument("--twopass", action="store_true",
+                    help="also time the checksum on Algorithm 1 (two passes over the keys), "
+                         "interleaved with the one-pass kernel")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--ramp-ms", type=float, default=300.0,
                     help="untimed launches for at least this long before the timed block "
@@ -358,6 +361,9 @@ def main():
     def off():
         F.attn_fwd(q, k, v, causal=w.causal, scale=w.scale, check=False, out=(o,))
 
+    def twopass():
+        F.attn_fwd_twopass(q, k, v, causal=w.causal, scale=w.scale, out=(o, resid, flags))
+
     # fault-free check first: counting the flags waits on the host, and the
     # GPU lowers its clock while idle, so the warmup runs last, right before
     # the timing
@@ -404,6 +410,24 @@ def main():
         off_ms.append(t_off / k_round)
         off_per += per_off
         ratios.append(t_on / t_off)
+    tp = None
+    if args.twopass:
+        twopass()
+        torch.cuda.synchronize()
+        tp_flagged = int((flags != 0).sum())
+        tp_ms, tp_ratio = [], []
+        for r in range(args.rounds):
+            t_on, _ = time_launches(on, k_round, stream)
+            t_tp, _ = time_launches(twopass, k_round, stream)
+            tp_ms.append(t_tp / k_round)
+            tp_ratio.append(t_tp / t_on)
+        m_tp = sorted(tp_ms)[len(tp_ms) // 2]
+        tp = {"ms_per_step": round(m_tp, 5), "tflops": round(flops / (m_tp * 1e-3) / 1e12, 2),
+              "vs_one_pass": round(sorted(tp_ratio)[len(tp_ratio) // 2], 4),
+              "fault_free_flagged_rows": tp_flagged}
+        log(f"[bench] two passes (Algorithm 1): {m_tp:.4f} ms/step, {tp['tflops']:.1f} TFLOP/s "
+            f"(the attention flops), {tp['vs_one_pass']:.3f}x the one-pass time; "
+            f"flagged rows {tp_flagged}")
     sclk.pause()
     ratios.sort()
     overhead = 100.0 * (ratios[len(ratios) // 2] - 1.0)
@@ -449,7 +473,7 @@ def main():
                 "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": traffic,
                 "kernel": (f"fabft::fwd_kernel<{128 if w.d == 96 else w.d}, "
                            f"{str(w.causal).lower()}, true, false, "
-                           f"false, false, false>"),
+                           f"false, false, false, false>"),
                 "avg_launch_ms": round(avg_launch_ms, 5)}
 
     if args.copy_probe_mib > 0:
@@ -489,6 +513,7 @@ def main():
         "cache": (f"hot: launches back to back (working set {w_bytes(w) / 1e6:.0f} MB against "
                   f"the 256 MB Infinity Cache)"),
         "cold_cache": cold,
+        "twopass": tp,
         "roofline": roofline,
         "cpu_baseline": cpu,
     }
