@@ -64,6 +64,10 @@
 //    p <= 256 and o, l, c are rescaled (alpha != 1) rarely; o*alpha is
 //    skipped when no lane of the wave moved its max. o/l and c/l are
 //    unchanged in exact arithmetic (the shift cancels).
+//  * Algorithm 1 as the host of the checksum (optional): a first pass loads
+//    K only and takes each row's max score over all its keys; the second is
+//    the loop above with the running max preset to that value, so alpha
+//    stays 1 and nothing is rescaled.
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -338,6 +342,8 @@ struct StageId {
 // WCHK: the weighted second checksum is compiled in (only with CHECK).
 // SPLIT: the workgroup runs one key split and writes partial row states.
 // SCHK: the score check is compiled in (only with CHECK, not with SPLIT).
+// TWOPASS: Algorithm 1 hosts the checksum: a first pass over K takes each
+// row's max, the second runs the loop with that max fixed (only with CHECK).
 template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false,
           bool TWOPASS = false>
 __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(FwdParams p) {
