@@ -71,7 +71,7 @@ def test_bad_out_tensors_are_refused(qkv):
 
 @pytest.mark.parametrize("d", [64, 96, 128, 256])
 @pytest.mark.parametrize("Lk", [77, 1000])
-@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("split", [False, True, "twopass"])
 @pytest.mark.parametrize("causal", [False, True])
 def test_rows_past_the_keys_are_never_read(d, Lk, split, causal):
     """K and V of one head at the very end of a buffer with 64 NaN rows after
@@ -91,7 +91,11 @@ def test_rows_past_the_keys_are_never_read(d, Lk, split, causal):
 
     k, v = tailed(inp.k), tailed(inp.v)
     assert torch.isnan(k.reshape(-1)[-1:]).sum() == 0
-    if split:
+    if split == "twopass":
+        # both passes, the first one loading K alone
+        o, resid, flags = F.attn_fwd_twopass(q, k, v, causal=causal, scale=w.scale)
+        pred = None
+    elif split:
         o, resid, flags = F.attn_fwd_splitkv(q, k, v, causal=causal, scale=w.scale, nsplit=3)
         pred = None
     else:
