@@ -29,7 +29,7 @@ def _col_mean_f64(v):
 
 
 @pytest.mark.parametrize("d", [64, 128, 256])
-@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("split", [False, True, "twopass"])
 def test_uniform_weights_at_the_largest_key_length(d, split):
     Lk, Lq = _max_lk(d), 3
     print(f"[maxsize] d={d} Lk={Lk} split={split}", flush=True)
@@ -37,7 +37,9 @@ def test_uniform_weights_at_the_largest_key_length(d, split):
     q = torch.randn((1, 1, Lq, d), generator=g, device="cuda").to(torch.bfloat16)
     k = torch.zeros((1, 1, Lk, d), dtype=torch.bfloat16, device="cuda")
     v = torch.randn((1, 1, Lk, d), generator=g, device="cuda").to(torch.bfloat16)
-    if split:
+    if split == "twopass":
+        o, resid, flags = F.attn_fwd_twopass(q, k, v, causal=False, scale=d ** -0.5)
+    elif split:
         o, resid, flags = F.attn_fwd_splitkv(q, k, v, causal=False, scale=d ** -0.5)
     else:
         o, resid, flags = F.attn_fwd(q, k, v, causal=False, scale=d ** -0.5)
