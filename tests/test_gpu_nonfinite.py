@@ -24,13 +24,17 @@ def _bits(t):
 
 @pytest.mark.parametrize("w", CASES, ids=[c.name for c in CASES])
 @pytest.mark.parametrize("row", [5, 100])
-@pytest.mark.parametrize("check", [True, False])
+@pytest.mark.parametrize("check", [True, False, "twopass"])
 def test_nan_query_row_stays_in_its_row(w, row, check):
     print(f"[nonfinite] {w.name} row {row} check {check}", flush=True)
     q, k, v = G.dev_inputs(W.make_inputs(w))
     qn = q.clone()
     qn[0, 1, row, 7] = float("nan")
-    if check:
+    if check == "twopass":
+        # the NaN row's first pass finds no finite max; its second pass stays NaN
+        o0, r0, f0 = F.attn_fwd_twopass(q, k, v, causal=w.causal, scale=w.scale)
+        o, r, f = F.attn_fwd_twopass(qn, k, v, causal=w.causal, scale=w.scale)
+    elif check:
         o0, r0, f0 = F.attn_fwd(q, k, v, causal=w.causal, scale=w.scale)
         o, r, f = F.attn_fwd(qn, k, v, causal=w.causal, scale=w.scale)
     else:
