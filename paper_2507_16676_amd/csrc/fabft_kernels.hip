@@ -1373,8 +1373,253 @@ int launch_merge(const FwdParams& p, int d, int nheads, hipStream_t stream) {
   return hipGetLastError() == hipSuccess ? 0 : -1;
 }
 
+// ---- key split for a few query rows (Lq <= 4, decode): the MFMA kernel
+// keeps one wave of its workgroup busy on a 32-row block whose other rows
+// are empty, and that wave's tile work, not HBM, then sets the pace. Here
+// every wave streams its own keys from HBM into registers and takes the
+// products on the vector ALU: lane (g, c) of a load holds the 16-byte chunk
+// c of key g's row (LPK = D / 8 lanes per key), so q . k is four dot2 per
+// lane and a sum over the key's LPK lanes, and the P V update is eight FMAs
+// per lane into the lane's own eight columns. Per row and wave: a running
+// max (lazily moved, as in the forward kernel), l, c = sum p sumrow(V) (and
+// c_w) and o, all in fp32 on the same p (Alg. 3); the waves' states are
+// merged through LDS into the split's partial-state record, which
+// merge_kernel combines across splits and checks as for the MFMA kernel.
+constexpr int kDecWaves = 8;
+constexpr int kDecLoads = 4;   // loads of K (and of V) per wave step
+constexpr int kDecMaxRows = 4; // query rows per head up to which a split takes this kernel
+
+// sum / max over aligned groups of N (8, 16, 32 or 64) lanes
+template <int N>
+__device__ __forceinline__ float span_sum(float x) {
+  static_assert(N == 8 || N == 16 || N == 32 || N == 64, "span");
+  x = group_sum<8>(x);
+  if constexpr (N >= 16) x += dpp<0x140>(x);   // row_mirror: lanes i and 15 - i
+  if constexpr (N >= 32) x += __shfl_xor(x, 16);
+  if constexpr (N == 64) x = sum_xor32(x);
+  return x;
+}
+// combine over the lanes that differ only in bits log2(G) .. 5 (the groups)
+template <int G>
+__device__ __forceinline__ float groups_sum(float x) {
+#pragma unroll
+  for (int o = G; o < 64; o <<= 1) x += __shfl_xor(x, o);
+  return x;
+}
+template <int G>
+__device__ __forceinline__ float groups_max(float x) {
+#pragma unroll
+  for (int o = G; o < 64; o <<= 1) x = __builtin_fmaxf(x, __shfl_xor(x, o));
+  return x;
+}
+
+template <int D, int NQ, bool CAUSAL, bool WCHK>
+__global__ __launch_bounds__(64 * kDecWaves) void decode_kernel(FwdParams p) {
+  constexpr int LPK = D / 8;                // lanes per key
+  constexpr int KPL = 64 / LPK;             // keys per load
+  constexpr int NL = kDecLoads;
+  constexpr int KS = NL * KPL;              // keys per wave step
+  constexpr int R = D + 4;                  // record floats
+  __shared__ float red[kDecWaves][NQ][R];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int split = blockIdx.x % p.nsplit;
+  const int bh = blockIdx.x / p.nsplit;     // one query tile per head (Lq <= 4)
+  const int Lq = p.Lq, Lk = p.Lk, off = Lk - Lq;
+  const int DIO = p.dio, CIO = DIO / 8;
+  const int c = lane % LPK, kg = lane / LPK;
+  const float sl2 = p.sl2;
+  // the split's keys: whole key tiles, as in the MFMA split kernel
+  const int ntiles = (Lk + kBc - 1) / kBc;
+  const int t_lo = min(ntiles, split * p.split_tiles);
+  const int k_lo = t_lo * kBc;
+  const int k_hi = min(Lk, min(ntiles, t_lo + p.split_tiles) * kBc);
+  const int nsteps = (k_hi - k_lo + KS - 1) / KS;
+  const bool col_ok = c < CIO;
+  const uint16_t* kh = p.k + (size_t)bh * Lk * DIO + 8 * c;
+  const uint16_t* vh = p.v + (size_t)bh * Lk * DIO + 8 * c;
+
+  u32x4 q[NQ];
+#pragma unroll
+  for (int r = 0; r < NQ; ++r) {
+    q[r] = u32x4{0, 0, 0, 0};
+    if (r < Lq && col_ok)
+      q[r] = *reinterpret_cast<const u32x4*>(p.q + ((size_t)bh * Lq + r) * DIO + 8 * c);
+  }
+  float m2[NQ], l[NQ], cs[NQ], cw[NQ], o[NQ][8];
+#pragma unroll
+  for (int r = 0; r < NQ; ++r) {
+    m2[r] = -__builtin_inff();
+    l[r] = cs[r] = cw[r] = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) o[r][j] = 0.f;
+  }
+
+  // keys of step j: k_lo + j*KS + n*KPL + kg (n < NL); rows past k_hi and
+  // chunks past the row's DIO columns load as zeros
+  auto load = [&](int j, u32x4 (&kk)[NL], u32x4 (&vv)[NL]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int n = 0; n < NL; ++n) {
+      const int key = k_lo + j * KS + n * KPL + kg;
+      kk[n] = u32x4{0, 0, 0, 0};
+      vv[n] = u32x4{0, 0, 0, 0};
+      if (j < nsteps && key < k_hi && col_ok) {
+        kk[n] = *reinterpret_cast<const u32x4*>(kh + (size_t)key * DIO);
+        vv[n] = *reinterpret_cast<const u32x4*>(vh + (size_t)key * DIO);
+      }
+    }
+  };
+  auto step = [&](int j, const u32x4 (&kk)[NL], const u32x4 (&vv)[NL]) __attribute__((always_inline)) {
+    if (j >= nsteps) return;   // wave-uniform
+    // sumrow(V) (and the weighted sum) of each key of the step (Eq. 4)
+    float vs[NL], vw[NL];
+#pragma unroll
+    for (int n = 0; n < NL; ++n) {
+      float a = 0.f, b = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        a = dot2(vv[n][e], kOnes, a);
+        if constexpr (WCHK) b = dot2(vv[n][e], kAlt, b);
+      }
+      vs[n] = span_sum<LPK>(a);
+      vw[n] = WCHK ? span_sum<LPK>(b) : 0.f;
+    }
+    float vf[NL][8];
+#pragma unroll
+    for (int n = 0; n < NL; ++n)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        vf[n][2 * e] = __uint_as_float(vv[n][e] << 16);
+        vf[n][2 * e + 1] = __uint_as_float(vv[n][e] & 0xffff0000u);
+      }
+#pragma unroll
+    for (int r = 0; r < NQ; ++r) {
+      // s = q . k (Alg. 3), -inf where the key is not visible to row r
+      float sc[NL];
+      float mx = -__builtin_inff();
+#pragma unroll
+      for (int n = 0; n < NL; ++n) {
+        float a = 0.f;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a = dot2(q[r][e], kk[n][e], a);
+        a = span_sum<LPK>(a);
+        const int key = k_lo + j * KS + n * KPL + kg;
+        const bool vis = key < k_hi && r < Lq && (!CAUSAL || key <= r + off);
+        sc[n] = vis ? a : -__builtin_inff();
+        mx = __builtin_fmaxf(mx, sc[n]);
+      }
+      mx = groups_max<LPK>(mx);
+      // lazy running max in the exp2 domain
+      const float mt2 = (mx == -__builtin_inff()) ? -__builtin_inff() : mx * sl2;
+      const float m2n = (mt2 > m2[r] + kLazy) ? mt2 : m2[r];
+      if (m2n != m2[r]) {   // wave-uniform
+        const float alpha = __builtin_amdgcn_exp2f(m2[r] - m2n);
+        l[r] *= alpha;
+        cs[r] *= alpha;
+        cw[r] *= alpha;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) o[r][jj] *= alpha;
+        m2[r] = m2n;
+      }
+      const float nm2 = (m2n == -__builtin_inff()) ? 0.f : -m2n;
+#pragma unroll
+      for (int n = 0; n < NL; ++n) {
+        const float pr = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[n], sl2, nm2));
+        l[r] += pr;
+        cs[r] = __builtin_fmaf(pr, vs[n], cs[r]);
+        if constexpr (WCHK) cw[r] = __builtin_fmaf(pr, vw[n], cw[r]);
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) o[r][jj] = __builtin_fmaf(pr, vf[n][jj], o[r][jj]);
+      }
+    }
+  };
+
+  // three steps in flight per wave: this wave's steps are wave, wave + W, ...
+  u32x4 k0[NL], v0[NL], k1[NL], v1[NL], k2[NL], v2[NL];
+  constexpr int W = kDecWaves;
+  load(wave, k0, v0);
+  load(wave + W, k1, v1);
+  for (int j = wave; j < nsteps; j += 3 * W) {
+    load(j + 2 * W, k2, v2);
+    step(j, k0, v0);
+    load(j + 3 * W, k0, v0);
+    step(j + W, k1, v1);
+    load(j + 4 * W, k1, v1);
+    step(j + 2 * W, k2, v2);
+  }
+
+  // the wave's state per row: l, c, c_w and o summed over its key groups
+  // (every lane of a group holds its group's sums), then through LDS
+#pragma unroll
+  for (int r = 0; r < NQ; ++r) {
+    l[r] = groups_sum<LPK>(l[r]);
+    cs[r] = groups_sum<LPK>(cs[r]);
+    cw[r] = groups_sum<LPK>(cw[r]);
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) o[r][jj] = groups_sum<LPK>(o[r][jj]);
+    if (kg == 0) {
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) red[wave][r][4 + 8 * c + jj] = o[r][jj];
+    }
+    if (lane == 0) {
+      red[wave][r][0] = m2[r];
+      red[wave][r][1] = l[r];
+      red[wave][r][2] = cs[r];
+      red[wave][r][3] = cw[r];
+    }
+  }
+  __syncthreads();
+  // merge of the waves (m = max_w m_w, x = sum_w x_w 2^(m_w - m)) into the
+  // split's record; a split without a visible key keeps m = -inf, weight 0
+  for (int e = tid; e < NQ * R; e += 64 * kDecWaves) {
+    const int r = e / R, idx = e - r * R;
+    if (r >= Lq) continue;
+    float mm = -__builtin_inff();
+#pragma unroll
+    for (int w = 0; w < kDecWaves; ++w) mm = __builtin_fmaxf(mm, red[w][r][0]);
+    float x = mm;
+    if (idx > 0) {
+      x = 0.f;
+      if (mm != -__builtin_inff()) {
+#pragma unroll
+        for (int w = 0; w < kDecWaves; ++w)
+          x = __builtin_fmaf(__builtin_amdgcn_exp2f(red[w][r][0] - mm), red[w][r][idx], x);
+      }
+    }
+    p.ws[(((size_t)bh * Lq + r) * p.nsplit + split) * R + idx] = x;
+  }
+}
+
+template <int D, bool CAUSAL>
+static int launch_decode_c(const FwdParams& p, hipStream_t s) {
+  const dim3 grid(p.grid), block(64 * kDecWaves);
+  (void)hipGetLastError();
+  const bool w = p.wcheck != 0;
+  if (p.Lq == 1) {
+    if (w) hipLaunchKernelGGL((decode_kernel<D, 1, CAUSAL, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((decode_kernel<D, 1, CAUSAL, false>), grid, block, 0, s, p);
+  } else if (p.Lq == 2) {
+    if (w) hipLaunchKernelGGL((decode_kernel<D, 2, CAUSAL, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((decode_kernel<D, 2, CAUSAL, false>), grid, block, 0, s, p);
+  } else {
+    if (w) hipLaunchKernelGGL((decode_kernel<D, 4, CAUSAL, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((decode_kernel<D, 4, CAUSAL, false>), grid, block, 0, s, p);
+  }
+  return hipGetLastError() == hipSuccess ? 0 : -1;
+}
+
+template <int D>
+static int launch_decode(const FwdParams& p, bool causal, hipStream_t s) {
+  return causal ? launch_decode_c<D, true>(p, s) : launch_decode_c<D, false>(p, s);
+}
+
 int launch_fwd(const FwdParams& p, int d, bool causal, int mode, hipStream_t stream) {
   const int dc = compute_width(d);
+  if (mode == 3 && p.Lq <= kDecMaxRows && p.n_qt == 1) {
+    // a key split of at most four query rows: the vector-ALU decode kernel
+    if (dc == 256) return launch_decode<256>(p, causal, stream);
+    if (dc == 128) return launch_decode<128>(p, causal, stream);
+    return launch_decode<64>(p, causal, stream);
+  }
   if (dc == 256) return launch_d<256>(p, causal, mode, stream);
   if (dc == 128) return launch_d<128>(p, causal, mode, stream);
   return launch_d<64>(p, causal, mode, stream);

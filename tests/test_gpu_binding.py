@@ -71,14 +71,16 @@ def test_bad_out_tensors_are_refused(qkv):
 
 @pytest.mark.parametrize("d", [64, 96, 128, 256])
 @pytest.mark.parametrize("Lk", [77, 1000])
-@pytest.mark.parametrize("split", [False, True, "twopass"])
+@pytest.mark.parametrize("split", [False, True, "twopass", "decode"])
 @pytest.mark.parametrize("causal", [False, True])
 def test_rows_past_the_keys_are_never_read(d, Lk, split, causal):
     """K and V of one head at the very end of a buffer with 64 NaN rows after
     them (the last key tile reads up to 63 rows past Lk, which must come back
     as zeros): O matches the oracle and no row is flagged. Every read stays
     inside the buffer, so a wrong bound shows as NaN, not as a fault."""
-    w = W.Workload(f"tail{Lk}", 1, 1, 150, Lk, d, causal, d ** -0.5, seed=Lk + d)
+    # "decode": two query rows, the key split's vector-ALU decode kernel
+    Lq = 2 if split == "decode" else 150
+    w = W.Workload(f"tail{Lk}", 1, 1, Lq, Lk, d, causal, d ** -0.5, seed=Lk + d)
     print(f"[tail] Lk={Lk} d={d} split={split} causal={causal}", flush=True)
     inp = W.make_inputs(w)
     q = G.to_dev(inp.q)
@@ -95,7 +97,7 @@ def test_rows_past_the_keys_are_never_read(d, Lk, split, causal):
         # both passes, the first one loading K alone
         o, resid, flags = F.attn_fwd_twopass(q, k, v, causal=causal, scale=w.scale)
         pred = None
-    elif split:
+    elif split:   # the MFMA split kernel, or the decode kernel for two rows
         o, resid, flags = F.attn_fwd_splitkv(q, k, v, causal=causal, scale=w.scale, nsplit=3)
         pred = None
     else:

@@ -1,8 +1,9 @@
 """Key-split forward (partial states per key range and a merge that carries
 the checksum c like one more column of o) on the GPU through the C ABI:
-decode-shaped inputs (few queries, many keys), empty splits, d = 64 and
-128, causal and not; O against the fp64 oracle, no flags fault-free, the
-residual as small as in the one-pass kernel."""
+decode-shaped inputs (few queries, many keys; up to four rows take the
+vector-ALU decode kernel, more the MFMA split kernel), empty splits,
+d = 64, 96, 128 and 256, causal and not; O against the fp64 oracle, no
+flags fault-free, the residual as small as in the one-pass kernel."""
 import numpy as np
 import pytest
 import torch
@@ -23,6 +24,14 @@ CASES = [
     (W.Workload("one", 1, 1, 5, 2000, 64, False, 0.125, seed=15), 1),
     (W.Workload("dec3d96", 2, 2, 3, 1500, 96, True, 96 ** -0.5, seed=16), 6),
     (W.Workload("dec5d256", 1, 3, 5, 2100, 256, True, 256 ** -0.5, seed=17), 7),
+    # up to four query rows: the vector-ALU decode kernel (ragged key counts,
+    # causal rows that see different key counts, splits with no key)
+    (W.Workload("dec1d64", 2, 3, 1, 3001, 64, False, 0.125, seed=18), 5),
+    (W.Workload("dec2c", 1, 4, 2, 2500, 128, True, 128 ** -0.5, seed=19), 7),
+    (W.Workload("dec4c256", 1, 2, 4, 1111, 256, True, 256 ** -0.5, seed=20), 3),
+    (W.Workload("dec4d96", 2, 2, 4, 700, 96, False, 96 ** -0.5, seed=21), 11),
+    (W.Workload("dec1e", 1, 2, 1, 100, 128, False, 128 ** -0.5, seed=22), 8),
+    (W.Workload("dec3c64", 1, 3, 3, 4099, 64, True, 0.125, seed=23), 2),
 ]
 
 
@@ -60,6 +69,23 @@ def test_splitkv_weighted():
         assert int((flags != 0).sum()) == 0
     finally:
         F.set_weighted_check(False)
+
+
+def test_splitkv_weighted_decode():
+    """The weighted check in the decode kernel (two rows, causal): no flag,
+    and O is the same with the check on and off."""
+    w, ns = CASES[8]
+    assert w.Lq <= 4
+    q, k, v = G.dev_inputs(W.make_inputs(w))
+    o0, r0, f0 = F.attn_fwd_splitkv(q, k, v, causal=w.causal, scale=w.scale, nsplit=ns)
+    F.set_weighted_check(True)
+    try:
+        o1, r1, f1 = F.attn_fwd_splitkv(q, k, v, causal=w.causal, scale=w.scale, nsplit=ns)
+        torch.cuda.synchronize()
+    finally:
+        F.set_weighted_check(False)
+    assert int((f0 != 0).sum()) == 0 and int((f1 != 0).sum()) == 0
+    assert torch.equal(o0.view(torch.int16), o1.view(torch.int16))
 
 
 def test_splitkv_workspace_reused():
