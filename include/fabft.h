@@ -134,7 +134,9 @@ long long fabft_splitkv_workspace_bytes(int B, int H, int Lq, int d, int nsplit)
  * more column of o (Eq. 10) -- and applies the per-row check after the
  * merge, so faults in the merge of o are covered too. O, resid and flags
  * have the same meaning and layout as in fabft_attn_fwd; results match it to
- * rounding (not bitwise). workspace: device memory of at least
+ * rounding (not bitwise). With Lq <= 4 the ranges run on the vector ALU
+ * (every wave streams its own keys; p stays fp32 for both o and c), with
+ * more rows on the matrix cores as in fabft_attn_fwd. workspace: device memory of at least
  * fabft_splitkv_workspace_bytes(B, H, Lq, d, nsplit) bytes, 16-byte aligned,
  * owned by the caller, overwritten. nsplit: 1..64. Asynchronous (two
  * launches in order on the library stream).
