@@ -32,6 +32,11 @@ CASES = [
     (W.Workload("dec4d96", 2, 2, 4, 700, 96, False, 96 ** -0.5, seed=21), 11),
     (W.Workload("dec1e", 1, 2, 1, 100, 128, False, 128 ** -0.5, seed=22), 8),
     (W.Workload("dec3c64", 1, 3, 3, 4099, 64, True, 0.125, seed=23), 2),
+    # 1% of the keys scaled by 8: scores that jump past the lazily kept max
+    # late in a wave's keys, so the decode kernel rescales l, c and o
+    (W.Workload("dec2peak", 1, 4, 2, 6000, 128, True, 128 ** -0.5, peaked_frac=0.01,
+                seed=24), 3),
+    (W.Workload("dec1peak64", 2, 2, 1, 5000, 64, False, 0.125, peaked_frac=0.01, seed=25), 4),
 ]
 
 
