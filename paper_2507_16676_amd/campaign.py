@@ -368,13 +368,21 @@ def summarize(path):
             "paper_table_by_nfaults": {k: paper_table(v) for k, v in sorted(by_k.items())}}
 
 
-def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000, score_check=False):
+def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000, score_check=False,
+              path="forward"):
     """Fault-free runs on seeds seed0..seed0+seeds-1: count flagged rows
     (must be 0) and track rho = max |resid| / (sum_j |O_ij| + |pred|), and
     with the weighted check on, the same ratio for it (rho_w). score_check
-    records that the caller switched the score check on (its flags count)."""
+    records that the caller switched the score check on (its flags count).
+    path: "forward" (fabft_attn_fwd), "splitkv" (the key split with its
+    default split count) or "twopass" (the checksum on Algorithm 1); the two
+    latter have no debug outputs, so their rho takes pred = resid + sum_j O_ij
+    from the bf16 O."""
     torch = _torch()
-    from . import attn_fwd, attn_fwd_inject, get_threshold, get_weighted_check
+    from . import (attn_fwd, attn_fwd_inject, attn_fwd_splitkv, attn_fwd_twopass, get_threshold,
+                   get_weighted_check)
+    if path not in ("forward", "splitkv", "twopass"):
+        raise ValueError(f"unknown path {path!r}")
     weighted = get_weighted_check()
     rho_w_max = 0.0
     o = resid = flags = None
@@ -385,12 +393,22 @@ def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000, score_
     for i in range(seeds):
         s = seed0 + i
         q, k, v = device_inputs(w, s)
-        o, resid, flags = attn_fwd(q, k, v, causal=w.causal, scale=w.scale)
+        if path == "splitkv":
+            o, resid, flags = attn_fwd_splitkv(q, k, v, causal=w.causal, scale=w.scale)
+        elif path == "twopass":
+            o, resid, flags = attn_fwd_twopass(q, k, v, causal=w.causal, scale=w.scale)
+        else:
+            o, resid, flags = attn_fwd(q, k, v, causal=w.causal, scale=w.scale)
         nf = int((flags != 0).sum())
         if nf:
             flagged_total += nf
             flagged_seeds.append(s)
-        if rho_every and i % rho_every == 0:
+        if rho_every and i % rho_every == 0 and path != "forward":
+            of = o.float()
+            M = of.abs().sum(dim=-1) + (resid + of.sum(dim=-1)).abs()
+            rho_max = max(rho_max, (resid.abs() / M.clamp_min(1e-30)).max().item())
+            rho_seeds += 1
+        elif rho_every and i % rho_every == 0:
             od, rd, fd, pred, actual, pw, aw = attn_fwd_inject(
                 q, k, v, causal=w.causal, scale=w.scale, weighted_out=True)
             absO = od.float().abs().sum(dim=-1)
@@ -408,7 +426,7 @@ def run_sweep(w, seeds, out_path, seed0=1, rho_every=100, log_every=1000, score_
     res = {"workload": w.name, "seeds": seeds, "seed0": seed0, "rows_checked": rows,
            "flagged_rows": flagged_total, "flagged_seeds": flagged_seeds[:100],
            "rho_max": rho_max, "rho_seeds": rho_seeds, "threshold": get_threshold(),
-           "weighted_check": weighted, "score_check": bool(score_check),
+           "weighted_check": weighted, "score_check": bool(score_check), "path": path,
            "seconds": time.time() - t0}
     if weighted:
         res["rho_w_max"] = rho_w_max
@@ -452,6 +470,8 @@ def main(argv=None):
                    help="also run the weighted (alternating-sign) checksum")
     s.add_argument("--score-check", action="store_true",
                    help="also run the score check (row sums of Q K^T); its flags count too")
+    s.add_argument("--path", default="forward", choices=("forward", "splitkv", "twopass"),
+                   help="the entry point swept: the forward, the key split or the two-pass form")
     a = ap.parse_args(argv)
     w = W.WORKLOADS[a.workload]
     if a.weighted:
@@ -493,7 +513,7 @@ def main(argv=None):
                              device="cuda")
             set_score_check(ws)
         print(json.dumps(run_sweep(w, a.seeds, a.out, seed0=a.seed0, rho_every=a.rho_every,
-                                   score_check=a.score_check)))
+                                   score_check=a.score_check, path=a.path)))
 
 
 if __name__ == "__main__":

@@ -120,6 +120,9 @@ WORKLOADS = {
     "t1_dec_d128": Workload("t1_dec_d128", 1, 32, 256, 256, 128, True,
                             1.0 / math.sqrt(128.0)),
     "t1_dec_d256": Workload("t1_dec_d256", 1, 16, 256, 256, 256, True, 1.0 / 16.0),
+    # decode: one new query per head over a 32768-key cache (the key split's shape)
+    "decode_l32768": Workload("decode_l32768", 4, 32, 1, 32768, 128, False,
+                              1.0 / math.sqrt(128.0)),
 }
 
 
