@@ -172,3 +172,9 @@ def test_multi_fault_draws_share_a_head_and_are_reproducible():
     assert ks == {1, 2, 3, 4, 5}
     # one fault per run reproduces the single-fault draw
     assert C.draw_faults(7, w, 64, 256) == [C.draw_fault(7, w, 64, 256)]
+
+
+def test_sweep_rejects_an_unknown_path():
+    """The sweep's entry-point choice is checked before any device work."""
+    with pytest.raises(ValueError):
+        C.run_sweep(W.WORKLOADS["bert_l128"], 1, None, path="nonsense")
