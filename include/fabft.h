@@ -17,9 +17,11 @@
  *    contiguous row-major [B, H, Lq, d] (q, o) and [B, H, Lk, d] (k, v),
  *    16-byte aligned. resid is fp32 [B, H, Lq], flags is uint8 [B, H, Lq],
  *    pred/actual (when given) fp32 [B, H, Lq]; all device pointers.
- *  - The caller owns every buffer. The library allocates nothing and keeps
- *    only a stream, the detection threshold and the weighted-check switch as
- *    process-global state (setters are not thread-safe).
+ *  - The caller owns every buffer. The library allocates nothing (one entry
+ *    point uses a static device array of its own instead of a workspace) and
+ *    keeps only a stream, the detection thresholds, the weighted- and
+ *    score-check switches and the launch shape as process-global state
+ *    (setters are not thread-safe).
  *  - d must be 64, 96, 128 or 256 (d = 96 runs the d = 128 kernels with the
  *    columns 96..127 zero on chip: identical results, 4/3 of the work).
  *    B, H, Lq, Lk >= 1. scale must be finite and >= 0; a scale below
@@ -36,6 +38,9 @@
  *  - Computation: bf16 MFMA with fp32 accumulation for Q K^T and P V; the
  *    softmax weights fed to P V are rounded to bf16 (p~), and the checksum
  *    uses exactly those p~; l, c, the row sums and the residual are fp32.
+ *    (The key split with at most four query rows computes both products on
+ *    the vector ALU in fp32 instead, with the same unrounded p for o, l
+ *    and c.)
  *  - Results are bitwise deterministic run to run for fixed inputs.
  */
 #ifndef FABFT_H
