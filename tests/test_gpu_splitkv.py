@@ -76,6 +76,24 @@ def test_splitkv_weighted():
         F.set_weighted_check(False)
 
 
+@pytest.mark.parametrize("d", [64, 128])
+def test_decode_rows_without_keys(d):
+    """Four causal rows over two keys: rows 0 and 1 see no key (bottom-right
+    alignment), so their O, resid and flags are 0; rows 2 and 3 match the
+    oracle."""
+    w = W.Workload("dec4short", 1, 2, 4, 2, d, True, d ** -0.5, seed=26)
+    inp = W.make_inputs(w)
+    q, k, v = G.dev_inputs(inp)
+    o, resid, flags = F.attn_fwd_splitkv(q, k, v, causal=True, scale=w.scale, nsplit=2)
+    torch.cuda.synchronize()
+    assert torch.all(o[:, :, :2].float() == 0)
+    assert torch.all(resid[:, :, :2] == 0)
+    assert int((flags != 0).sum()) == 0
+    ref = G.oracle_rows(inp, True, w.scale)
+    O = G.from_dev_bf16(o)
+    assert np.abs(O - ref["O"]).max() <= G.O_MAX_ABS
+
+
 def test_splitkv_weighted_decode():
     """The weighted check in the decode kernel (two rows, causal): no flag,
     and O is the same with the check on and off."""
