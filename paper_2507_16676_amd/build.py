@@ -45,15 +45,24 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 KERNEL_FLAGS = ["-mno-amdgpu-ieee", "-fno-honor-nans"]
 
 
+# The kernel source is compiled twice (FABFT_PART 0 and 1, see its head): the
+# second part, the d = 128 forward kernels without the weighted check, with
+# LLVM's iterative ILP scheduler.
+PART1_FLAGS = ["-DFABFT_PART=1", "-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]
+
+
 def build_cmds(out: str, objdir: str, extra=()) -> list[list[str]]:
     inc = ["-I", os.path.join(ROOT, "include")]
     hipcc = hipcc_path()
     k_obj = os.path.join(objdir, "fabft_kernels.o")
+    k1_obj = os.path.join(objdir, "fabft_kernels_part1.o")
     a_obj = os.path.join(objdir, "fabft_api.o")
     return [
         [hipcc, "-x", "hip", *COMMON, *KERNEL_FLAGS, *inc, *extra, "-c", SOURCES[0], "-o", k_obj],
+        [hipcc, "-x", "hip", *COMMON, *KERNEL_FLAGS, *PART1_FLAGS, *inc, *extra, "-c", SOURCES[0],
+         "-o", k1_obj],
         [hipcc, "-x", "hip", *COMMON, *inc, *extra, "-c", SOURCES[1], "-o", a_obj],
-        [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", k_obj, a_obj, "-o", out],
+        [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", k_obj, k1_obj, a_obj, "-o", out],
     ]
 
 
