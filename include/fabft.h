@@ -122,6 +122,19 @@ int fabft_attn_fwd_twopass(const void* q, const void* k, const void* v,
                            float scale);
 
 /*
+ * The algorithm that hosts the checksum in fabft_attn_fwd, the injection and
+ * debug entry points and fabft_recompute_flagged: 3 (Algorithm 3, one pass;
+ * the default) or 1 (Algorithm 1, the two passes of fabft_attn_fwd_twopass),
+ * so that a fault campaign can run on either form. Process-global, not
+ * thread-safe. fabft_set_algorithm returns FABFT_E_MODE for any other value;
+ * with Algorithm 1 selected, those entry points return FABFT_E_MODE while
+ * the score check is on. The key split and fabft_attn_fwd_nocheck are not
+ * affected.
+ */
+int fabft_set_algorithm(int alg);
+int fabft_get_algorithm(void);
+
+/*
  * Bytes of workspace that fabft_attn_fwd_splitkv needs: one partial-state
  * record of (w + 4) floats per (b, h, query row, split), w the compute width
  * (d, or 128 for d = 96). Negative status for d not 64, 96, 128 or 256, a size

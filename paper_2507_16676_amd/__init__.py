@@ -75,6 +75,10 @@ def _load() -> ctypes.CDLL:
     L.fabft_attn_fwd_nocheck.restype = _i
     L.fabft_attn_fwd_twopass.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f]
     L.fabft_attn_fwd_twopass.restype = _i
+    L.fabft_set_algorithm.argtypes = [_i]
+    L.fabft_set_algorithm.restype = _i
+    L.fabft_get_algorithm.argtypes = []
+    L.fabft_get_algorithm.restype = _i
     L.fabft_attn_fwd_inject.argtypes = [_vp, _vp, _vp, _vp, _vp, _vp, _i, _i, _i, _i, _i, _i,
                                         _f, ctypes.POINTER(FabftFault), _vp, _vp, _vp, _vp]
     L.fabft_attn_fwd_inject.restype = _i
@@ -140,6 +144,7 @@ EXPORTS = ("fabft_attn_fwd", "fabft_attn_fwd_nocheck", "fabft_attn_fwd_twopass",
            "fabft_global_check", "fabft_recompute_flagged",
            "fabft_set_weighted_check", "fabft_get_weighted_check",
            "fabft_set_persistent", "fabft_get_persistent",
+           "fabft_set_algorithm", "fabft_get_algorithm",
            "fabft_key_tile", "fabft_query_tile", "fabft_status_str")
 
 
@@ -222,6 +227,17 @@ def set_persistent(mode: int):
 
 def get_persistent() -> int:
     return int(_load().fabft_get_persistent())
+
+
+def set_algorithm(alg: int):
+    """The algorithm hosting the checksum in attn_fwd, the injection and
+    debug paths and recompute_flagged (process-global): 3 (one pass, the
+    default) or 1 (two passes, as attn_fwd_twopass)."""
+    _check(_load().fabft_set_algorithm(int(alg)), "fabft_set_algorithm")
+
+
+def get_algorithm() -> int:
+    return int(_load().fabft_get_algorithm())
 
 
 def key_tile(d: int) -> int:
@@ -539,7 +555,7 @@ __all__ = ["attn_fwd", "attn_fwd_twopass", "attn_fwd_inject", "attn_fwd_debug", 
            "global_check", "recompute_flagged", "Fault", "FabftError", "set_threshold",
            "set_score_check", "score_check_workspace_bytes", "get_score_threshold",
            "get_threshold", "set_weighted_check", "get_weighted_check", "set_persistent",
-           "get_persistent", "key_tile",
+           "get_persistent", "set_algorithm", "get_algorithm", "key_tile",
            "query_tile", "status_str", "lib", "LIB_PATH", "EXPORTS", "MAX_FAULTS", "FLAG_RESID",
            "FLAG_NONFINITE", "FLAG_WEIGHTED", "FLAG_SCORES", "PERSIST_OFF", "PERSIST_AUTO",
            "PERSIST_ALWAYS"]

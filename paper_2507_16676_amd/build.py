@@ -42,7 +42,12 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 # Kernels only: IEEE mode off, so max/min need no NaN-quieting of their inputs
 # (needs relaxed NaN rules; the kernels test non-finite values on the bits and
 # a NaN score still reaches exp2 and propagates into o, l and c).
-KERNEL_FLAGS = ["-mno-amdgpu-ieee", "-fno-honor-nans"]
+KERNEL_FLAGS = ["-mno-amdgpu-ieee", "-fno-honor-nans",
+                # the two-pass kernels unroll their loop over the two passes
+                # (each pass then has constant branches); the injection forms
+                # of that loop exceed LLVM's default size limit for a requested
+                # unroll, and rolled up they spill. No other kernel changes.
+                "-mllvm", "-pragma-unroll-threshold=100000"]
 
 
 # The kernel source is compiled twice (FABFT_PART 0 and 1, see its head): the

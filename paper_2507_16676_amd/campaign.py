@@ -460,6 +460,8 @@ def main(argv=None):
                         "(sites Q,O,M,L,C: the paper's per-query registers)")
     c.add_argument("--faults", default="1",
                    help="faults per run: K or KMIN-KMAX (drawn uniformly; one head per run)")
+    c.add_argument("--algorithm", type=int, default=3, choices=(1, 3),
+                   help="the algorithm hosting the checksum: 3 (one pass) or 1 (two passes)")
     s = sub.add_parser("sweep")
     s.add_argument("--workload", default="dec_l4096")
     s.add_argument("--seeds", type=int, default=10000)
@@ -474,6 +476,9 @@ def main(argv=None):
                    help="the entry point swept: the forward, the key split or the two-pass form")
     a = ap.parse_args(argv)
     w = W.WORKLOADS[a.workload]
+    if getattr(a, "algorithm", 3) != 3:
+        from . import set_algorithm
+        set_algorithm(a.algorithm)
     if a.weighted:
         from . import set_weighted_check
         set_weighted_check(True)

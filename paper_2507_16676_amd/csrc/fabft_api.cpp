@@ -45,6 +45,10 @@ void* g_sws = nullptr;
 long long g_sws_bytes = 0;
 constexpr float kTauScoreDefault = 1.0f / 4194304.0f;
 float g_tau_s = kTauScoreDefault;
+// Algorithm hosting the checksum in the checked one-pass entry points
+// (fabft_attn_fwd, the injection and debug entry points, recompute): 3 (one
+// pass, the default) or 1 (two passes: the row max first).
+int g_alg = 3;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kMaxSplits = 64;   // the merge reads one split per lane
@@ -119,10 +123,16 @@ long long score_ws_bytes(long long BH, int Lk, int d) {
   return 2 * fabft::kpre_floats(BH, Lk, d) * static_cast<long long>(sizeof(float));
 }
 
-// mode 0: no checksum; 1: checksum; 2: checksum + injection/debug. With the
-// score check switched on, modes 1 and 2 first write the K column sums of
-// the BH heads into its workspace.
+// mode 0: no checksum; 1: checksum; 2: checksum + injection/debug; 4: the
+// two-pass checksum. With Algorithm 1 selected, modes 1 and 2 run its
+// two-pass forms (4, 5); the score check runs in the one-pass kernels only.
+// With the score check switched on, modes 1 and 2 first write the K column
+// sums of the BH heads into its workspace.
 int launch(fabft::FwdParams p, int d, int causal, int mode, int BH) {
+  if (g_alg == 1 && (mode == 1 || mode == 2)) {
+    if (g_sws) return FABFT_E_MODE;
+    mode += 3;
+  }
   if (g_sws && (mode == 1 || mode == 2)) {
     if (d == 256) return FABFT_E_HEADDIM;
     if (score_ws_bytes(BH, p.Lk, d) > g_sws_bytes) return FABFT_E_WORKSPACE;
@@ -465,6 +475,14 @@ int fabft_set_persistent(int mode) {
 }
 
 int fabft_get_persistent(void) { return fabft::get_persistent(); }
+
+int fabft_set_algorithm(int alg) {
+  if (alg != 1 && alg != 3) return FABFT_E_MODE;
+  g_alg = alg;
+  return FABFT_OK;
+}
+
+int fabft_get_algorithm(void) { return g_alg; }
 
 int fabft_key_tile(int d) {
   if (!head_dim_ok(d)) return FABFT_E_HEADDIM;

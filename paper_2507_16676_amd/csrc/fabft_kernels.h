@@ -66,7 +66,8 @@ struct FwdParams {
 
 // mode 0: checksum off, 1: checksum on, 2: checksum on + debug/injection,
 // 3: checksum on, one key split per workgroup (partial states to p.ws),
-// 4: checksum on, two passes over the keys (Algorithm 1: the row max first).
+// 4: checksum on, two passes over the keys (Algorithm 1: the row max first),
+// 5: mode 4 with injection/debug outputs.
 // Modes 0 and 1 (without the score check) may run as many workgroups as fit
 // on the device at once, each running a list of items, when there are more
 // items than that (set_persistent: off, automatic, always).

@@ -606,7 +606,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
       // (lane grp holds columns 16s + 8grp .. +7 of its row)
       for (int fi = 0; fi < p.nf; ++fi) {
         const FaultDesc fd = p.f[fi];
-        if (fd.site == 8 && bh == fd.bh && qrow == fd.row && t == fd.tile &&
+        if (fd.site == 8 && pass == 1 && bh == fd.bh && qrow == fd.row && t == fd.tile &&
             ((fd.col >> 3) & 1) == grp) {
           const int sj = fd.col >> 4, e = (fd.col & 7) >> 1;
           const uint32_t mask = (1u << fd.bit) << (16 * (fd.col & 1));
@@ -644,7 +644,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
     if constexpr (INJECT) {
       for (int fi = 0; fi < p.nf; ++fi) {
         const FaultDesc fd = p.f[fi];
-        if (fd.site == 1 && bh == fd.bh && qrow == fd.row) {
+        if (fd.site == 1 && pass == 1 && bh == fd.bh && qrow == fd.row) {
           const int kl = fd.col - kv0;
           if (kl >= 0 && kl < BC && ((kl >> 3) & 1) == grp) {
             const int kb = kl >> 5, i = ((kl >> 4) & 1) * 8 + (kl & 7);
@@ -1007,7 +1007,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
           bool hit = false;
           for (int fi = 0; fi < p.nf; ++fi) {
             const FaultDesc fd = p.f[fi];
-            if ((fd.site == 4 || fd.site == 9) && bh == fd.bh && qt == fd.tile) {
+            if ((fd.site == 4 || fd.site == 9) && pass == 1 && bh == fd.bh && qt == fd.tile) {
               const int key = fd.row - t * BC;
               if (key >= 0 && key < BC) {
                 hit = true;
@@ -1254,12 +1254,14 @@ static int launch_t(const FwdParams& p0, hipStream_t stream) {
 }
 
 // mode 0: no checksum, 1: checksum, 2: checksum + injection/debug,
-// 3: checksum, key split, 4: checksum, two passes (Algorithm 1); the
-// weighted check (p.wcheck) in its own instantiations, below
+// 3: checksum, key split, 4: checksum, two passes (Algorithm 1), 5: the
+// same with injection/debug; the weighted check (p.wcheck) in its own
+// instantiations, below
 template <int D, bool CAUSAL>
 static int launch_c(const FwdParams& p, int mode, hipStream_t s) {
   if (mode == 0) return launch_t<D, CAUSAL, false, false, false, false>(p, s);
   if (mode == 4) return launch_t<D, CAUSAL, true, false, false, false, false, true>(p, s);
+  if (mode == 5) return launch_t<D, CAUSAL, true, true, false, false, false, true>(p, s);
   if constexpr (D != 256) {
     // the score check (not built for the one-wave-per-SIMD width 256)
     if (p.kpre && (mode == 1 || mode == 2)) {
@@ -1275,6 +1277,7 @@ static int launch_c(const FwdParams& p, int mode, hipStream_t s) {
 template <int D, bool CAUSAL>
 static int launch_c_weighted(const FwdParams& p, int mode, hipStream_t s) {
   if (mode == 4) return launch_t<D, CAUSAL, true, false, true, false, false, true>(p, s);
+  if (mode == 5) return launch_t<D, CAUSAL, true, true, true, false, false, true>(p, s);
   if constexpr (D != 256) {
     if (p.kpre && (mode == 1 || mode == 2)) {
       if (mode == 1) return launch_t<D, CAUSAL, true, false, true, false, true>(p, s);

@@ -112,6 +112,26 @@ def test_twopass_rejects_the_score_check():
         assert L.fabft_set_score_check(None, 0, 0.0) == F.FABFT_OK
 
 
+def test_algorithm_switch_validation():
+    L = F.lib()
+    assert L.fabft_get_algorithm() == 3
+    for bad in (0, 2, 4, -1):
+        assert L.fabft_set_algorithm(bad) == F.E_MODE
+    assert L.fabft_get_algorithm() == 3
+    try:
+        assert L.fabft_set_algorithm(1) == F.FABFT_OK
+        assert F.get_algorithm() == 1
+        # with Algorithm 1 selected the score check is refused before a launch
+        assert L.fabft_set_score_check(P, 1 << 20, 0.0) == F.FABFT_OK
+        try:
+            assert L.fabft_attn_fwd(P, P, P, P, P, P, 1, 2, 8, 8, 128, 1, 0.1) == F.E_MODE
+        finally:
+            assert L.fabft_set_score_check(None, 0, 0.0) == F.FABFT_OK
+    finally:
+        F.set_algorithm(3)
+    assert F.get_algorithm() == 3
+
+
 def test_nocheck_rejects_bad_arguments():
     lib = F.lib()
     assert lib.fabft_attn_fwd_nocheck(P, P, P, 0, 1, 1, 8, 8, 128, 0, 1.0) == F.E_NULL

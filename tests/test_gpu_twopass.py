@@ -147,3 +147,69 @@ def test_twopass_deterministic():
     torch.cuda.synchronize()
     assert torch.equal(a[0].view(torch.int16), b[0].view(torch.int16))
     assert torch.equal(a[1].view(torch.int32), b[1].view(torch.int32))
+
+
+def test_algorithm_switch_selects_the_two_pass_forms():
+    """With Algorithm 1 selected, attn_fwd and the debug path run the two-pass
+    kernels: the same O, resid and flags as attn_fwd_twopass, bit for bit;
+    the debug outputs give pred directly, which matches the oracle's
+    Algorithm 1 restatement."""
+    import oracle as O_
+    w = W.Workload("tp_switch", 1, 2, 333, 333, 128, True, 128 ** -0.5, seed=31)
+    inp = W.make_inputs(w)
+    q, k, v = G.dev_inputs(inp)
+    o2, r2, f2 = F.attn_fwd_twopass(q, k, v, causal=True, scale=w.scale)
+    try:
+        F.set_algorithm(1)
+        o, r, f = F.attn_fwd(q, k, v, causal=True, scale=w.scale)
+        od, rd, fd, pred, actual = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale)
+        torch.cuda.synchronize()
+    finally:
+        F.set_algorithm(3)
+    for a, b in ((o, o2), (od, o2)):
+        assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+    assert torch.equal(r.view(torch.int32), r2.view(torch.int32))
+    assert torch.equal(rd.view(torch.int32), r2.view(torch.int32))
+    assert int((f != 0).sum()) == 0 and int((fd != 0).sum()) == 0
+    qf, kf, vf = inp.as_f32()
+    for h in range(w.H):
+        ref = O_.lazy_softmax_attention(qf[0, h], kf[0, h], vf[0, h], True, w.scale)
+        P = pred[0, h].double().cpu().numpy()
+        assert np.abs(P - ref["pred"]).max() <= G.O_MAX_ABS * np.sqrt(w.d)
+        assert np.abs(P - ref["pred"]).sum() <= G.O_REL_L1 * np.abs(ref["pred"]).sum()
+
+
+@pytest.mark.parametrize("site,kw", [
+    ("P", dict(b=0, h=0, row=250, col=100, bit=14)),
+    ("O", dict(b=0, h=1, row=200, col=37, tile=2, bit=30)),
+    ("V", dict(b=0, h=1, row=100, col=5, tile=0, bit=14)),
+])
+def test_algorithm1_flags_injected_faults(site, kw):
+    """Exponent flips at P, O and V under Algorithm 1: only rows of the
+    faulted head change, and the rows whose output moved by more than 2^-8
+    of their largest value are flagged (the same bar as the one-pass
+    campaign)."""
+    w = W.Workload("tp_inject", 1, 2, 300, 300, 128, True, 128 ** -0.5, seed=7)
+    q, k, v = G.dev_inputs(W.make_inputs(w))
+    try:
+        F.set_algorithm(1)
+        o0, r0, f0, p0, a0 = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale)
+        o, r, f, p, a = F.attn_fwd_inject(q, k, v, causal=True, scale=w.scale,
+                                          fault=F.Fault(site, **kw))
+        torch.cuda.synchronize()
+    finally:
+        F.set_algorithm(3)
+    assert int((f0 != 0).sum()) == 0
+    moved = (o.view(torch.int16) != o0.view(torch.int16)).any(dim=-1)
+    assert bool(moved.any())
+    assert not bool(moved[0, 1 - kw["h"]].any())
+    O = G.from_dev_bf16(o)[0, kw["h"]]
+    O0 = G.from_dev_bf16(o0)[0, kw["h"]]
+    # a row whose output turned non-finite counts as moved (an exponent flip
+    # of an fp32 accumulator in [1, 2) makes it NaN or infinite)
+    dif = np.abs(O - O0)
+    dif[~np.isfinite(dif)] = np.inf
+    big = np.where(dif.max(axis=1) > 2 ** -8 * np.abs(O0).max(axis=1))[0]
+    assert len(big) > 0
+    flagged = set(int(i) for i in (f[0, kw["h"]] != 0).nonzero().flatten().cpu().numpy())
+    assert set(int(i) for i in big) <= flagged
