@@ -90,6 +90,16 @@ HOST_SANITIZE = [f for s in SANITIZERS for f in ("-Xarch_host", "-fsanitize=" + 
     "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer", "-g"]
 
 
+def _run_all(cmds, verbose):
+    """The compile steps (all but the last command) run side by side; the
+    link runs after them."""
+    from concurrent.futures import ThreadPoolExecutor
+    with ThreadPoolExecutor(max_workers=len(cmds) - 1) as ex:
+        for f in [ex.submit(_run, c, verbose) for c in cmds[:-1]]:
+            f.result()
+    _run(cmds[-1], verbose)
+
+
 def build_host_sanitized(out: str, verbose: bool = False) -> str:
     """libfabft.so with ASan and UBSan on the host code, written to `out`."""
     import tempfile
@@ -98,8 +108,7 @@ def build_host_sanitized(out: str, verbose: bool = False) -> str:
         link = cmds[-1]
         cmds[-1] = (link[:-2] + [f for s in SANITIZERS for f in ("-Xarch_host", "-fsanitize=" + s)]
                     + ["-shared-libsan"] + link[-2:])
-        for cmd in cmds:
-            _run(cmd, verbose)
+        _run_all(cmds, verbose)
     return out
 
 
@@ -108,8 +117,7 @@ def build(verbose: bool = False, extra=()) -> str:
     tmp = LIB + f".tmp{os.getpid()}"
     with tempfile.TemporaryDirectory(prefix="fabft_build_") as objdir:
         try:
-            for cmd in build_cmds(tmp, objdir, extra):
-                _run(cmd, verbose)
+            _run_all(build_cmds(tmp, objdir, extra), verbose)
         except Exception:
             if os.path.exists(tmp):
                 os.unlink(tmp)
