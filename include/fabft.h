@@ -285,7 +285,7 @@ int fabft_get_weighted_check(void);
 /*
  * Persistent workgroups (a launch shape, not part of the method). When on,
  * fabft_attn_fwd and fabft_attn_fwd_nocheck launch only as many workgroups
- * as the device holds at once (one per compute unit, two at d = 64) when
+ * as the device holds at once (one per compute unit) when
  * there are more (head, query tile) items than that, each workgroup running
  * a fixed list of items; the next item's Q and first key tiles load while
  * the current item's last tiles and its epilogue run. It applies without the
@@ -293,8 +293,9 @@ int fabft_get_weighted_check(void);
  * debug, injection or score-check paths. Results are bitwise the same
  * either way (each row is computed by the same instructions in the same
  * order). Modes: FABFT_PERSIST_OFF (one workgroup per item),
- * FABFT_PERSIST_AUTO (default: on for d = 96 and 128 when Lk <= 1024, where
- * a workgroup's start-up is a large part of its work), FABFT_PERSIST_ALWAYS.
+ * FABFT_PERSIST_AUTO (default: on for d = 64, 96 and 128 when Lk <= 1024,
+ * where a workgroup's start-up is a large part of its work),
+ * FABFT_PERSIST_ALWAYS.
  * fabft_set_persistent returns FABFT_E_MODE for any other value.
  * Process-global, not thread-safe.
  */
@@ -307,8 +308,8 @@ int fabft_get_persistent(void);
 int fabft_key_tile(int d);
 
 /* Number of query rows per workgroup for head dimension d (the unit of
- * fabft_fault.tile at the V and VS sites): 256 at d = 96 and 128, 128 at
- * d = 64 and 256; FABFT_E_HEADDIM for an unsupported d. */
+ * fabft_fault.tile at the V and VS sites): 256 at d = 64, 96 and 128, 128
+ * at d = 256; FABFT_E_HEADDIM for an unsupported d. */
 int fabft_query_tile(int d);
 
 /* Fault sites for the injection path (where a single bit is flipped). */

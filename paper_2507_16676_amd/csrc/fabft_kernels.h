@@ -9,7 +9,7 @@ namespace fabft {
 
 // Query rows per workgroup for head dimension d: 8 waves of 32 rows, or 4
 // waves at d = 256 (one wave per SIMD, for the register file of 512).
-constexpr int query_tile_for(int d) { return (d == 256 || d == 64) ? 128 : 256; }
+constexpr int query_tile_for(int d) { return d == 256 ? 128 : 256; }
 
 // One injected single-bit fault (site numbers and fields as fabft_fault,
 // with the head flattened to bh = b * H + h).

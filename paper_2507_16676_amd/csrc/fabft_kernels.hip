@@ -9,8 +9,8 @@
 // actual = sum_j O_ij.
 //
 // Dataflow. One workgroup = 8 waves = 256 query rows (one workgroup per CU,
-// two waves per SIMD; at d = 64, 4 waves and two workgroups per CU; at
-// d = 256, 4 waves and one); one wave = 32 rows; key tiles of 64 keys.
+// two waves per SIMD; at d = 256, 4 waves and one); one wave = 32 rows; key
+// tiles of 64 keys.
 //  * The 32x32x16 bf16 MFMA computes S^T = K Q^T (keys on the M side, the
 //    wave's 32 queries on the N side) and O^T = V^T P^T. With this
 //    orientation a lane holds values of a single query row, so the row max,
@@ -55,7 +55,7 @@
 //    registers; c and l come out the same either way.
 //  * Masking (causal diagonal tiles, the ragged last tile) sets a score to
 //    -inf, whose exponential is exactly 0.
-//  * Persistent launch (optional): one or two workgroups per CU each run a
+//  * Persistent launch (optional): one workgroup per CU runs a
 //    list of (head, query tile) items; when an item has a multiple of four
 //    key tiles, the next item's first tiles load into the ring during its
 //    last steps and its Q during the epilogue.
@@ -101,13 +101,14 @@ typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
 // Workgroup shape per row width D: WAVES waves of 32 query rows, an LDS ring
 // of STAGES key tiles, AHEAD of them loading while one is in use. D = 256
 // runs one wave per SIMD (512 registers for its 256-wide Q and o fragments)
-// and a 2-stage ring (64 KiB per stage). D = 64 runs 4 waves with the 4-stage
-// ring (69 KiB): two workgroups share a CU, so that one's start-up and last
-// tiles overlap the other's work (4% faster than 8 waves on 512-key rows,
-// where a workgroup sees only 8 key tiles).
+// and a 2-stage ring (64 KiB per stage). D = 64 runs 8 waves like D = 128
+// with a 4-stage ring of 69 KiB; sumrow there is taken once per key tile for
+// 256 query rows rather than twice for two 4-wave workgroups of 128 rows
+// each (7-8% faster with the checksum on 2,048- and 4,096-key rows; on
+// 512-key rows the persistent launch makes up for the longer start-up).
 template <int D>
 struct Cfg {
-  static constexpr int WAVES = (D == 256 || D == 64) ? 4 : 8;
+  static constexpr int WAVES = (D == 256) ? 4 : 8;
   static constexpr int THREADS = 64 * WAVES;
   static constexpr int BR = 32 * WAVES;
   static constexpr int STAGES = D == 256 ? 2 : 4;
@@ -355,7 +356,7 @@ struct StageId {
 // row's max, the second runs the loop with that max fixed (only with CHECK).
 template <int D, bool CAUSAL, bool CHECK, bool INJECT, bool WCHK, bool SPLIT, bool SCHK = false,
           bool TWOPASS = false>
-__global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(FwdParams p) {
+__global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
   constexpr int kWaves = Cfg<D>::WAVES;
   constexpr int kThreads = Cfg<D>::THREADS;
   constexpr int kBr = Cfg<D>::BR;
@@ -538,14 +539,14 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, D == 64 ? 2 : 1) void fwd_kernel(F
   };
 
   // ---- sumrow(V) of the tile in stage S (Eq. 4): TPK threads per key on
-  // the first SW waves. At D = 128 only waves 0-3 (one per SIMD) take it,
-  // four threads per key: every SIMD spends one wave's vector instructions
+  // the first SW waves. Only waves 0-3 (one per SIMD) take it, four threads
+  // per key: with 8 waves every SIMD spends one wave's vector instructions
   // on it rather than two (the sums are the same work either way; the
   // per-key reduction and the hi / lo split are paid once per four lanes
   // instead of eight).
   auto sumrow = [&](auto S_) __attribute__((always_inline)) {
     constexpr int S = decltype(S_)::value;
-    constexpr int SW = (D == 128) ? 4 : kWaves;   // waves taking part
+    constexpr int SW = 4;                         // waves taking part
     constexpr int TPK = 64 * SW / BC;             // threads per key
     constexpr int CPT = CPR / TPK;                // 16-byte chunks per thread
     static_assert(TPK * BC == 64 * SW && CPT * TPK == CPR, "sumrow covers the tile");
@@ -1228,18 +1229,16 @@ static int launch_t(const FwdParams& p0, hipStream_t stream) {
   FwdParams p = p0;
   p.persist = 0;
   if constexpr (!INJECT && !SPLIT && !SCHK && !TWOPASS && Cfg<D>::AHEAD >= 3) {
-    // one or two workgroups per CU (the occupancy the launch bounds give),
-    // a multiple of 8 so that workgroup b stays on XCD b mod 8; with the
-    // mask only for a head count divisible by 8 (the banded schedule)
-    // Automatic only for short rows at d = 96 and 128 (at most 16 key
-    // tiles), where a workgroup's start-up is a large part of its work;
-    // measured neutral at d = 64 and on long rows.
-    const int per_cu = D == 64 ? 2 : 1;
-    const int g = (device_cus(stream) * per_cu) & ~7;
+    // one workgroup per CU (the occupancy the launch bounds give), a
+    // multiple of 8 so that workgroup b stays on XCD b mod 8; with the mask
+    // only for a head count divisible by 8 (the banded schedule). Automatic
+    // only for short rows (at most 16 key tiles), where a workgroup's
+    // start-up is a large part of its work; measured neutral on long rows.
+    const int g = device_cus(stream) & ~7;
     const int heads = p.n_items / p.n_qt;
     const int mode = g_persist.load();
     const bool want = mode == kPersistAlways ||
-                      (mode == kPersistAuto && D != 64 && (p.Lk + kBc - 1) / kBc <= 16);
+                      (mode == kPersistAuto && (p.Lk + kBc - 1) / kBc <= 16);
     if (want && g >= 8 && p.n_items > g && (!CAUSAL || (heads & 7) == 0)) {
       p.persist = 1;
       p.grid = g;

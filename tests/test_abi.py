@@ -41,7 +41,7 @@ def test_key_and_query_tiles():
     assert F.key_tile(128) == 64
     assert F.key_tile(64) == 64
     assert F.query_tile(128) == 256 and F.query_tile(96) == 256
-    assert F.query_tile(256) == 128 and F.query_tile(64) == 128
+    assert F.query_tile(256) == 128 and F.query_tile(64) == 256
     assert F.lib().fabft_query_tile(80) == F.E_HEADDIM
     assert F.key_tile(96) == 64
     with pytest.raises(F.FabftError):
