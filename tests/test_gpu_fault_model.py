@@ -185,7 +185,7 @@ def test_injected_runs_match_the_fault_model():
 
 @pytest.mark.parametrize("d", [64, 96])
 def test_injected_runs_match_the_fault_model_other_widths(d):
-    """The same on d = 64 (128-row query tiles, two workgroups per CU) and
+    """The same on d = 64 (the 64-wide kernel, 256-row query tiles) and
     d = 96 (the 128-wide kernel with zero columns), 80 runs each."""
     w = W.Workload(f"fm_gpu{d}", 1, 2, 333, 400, d, True, d ** -0.5, seed=62 + d)
     tau, _ = F.get_threshold()
