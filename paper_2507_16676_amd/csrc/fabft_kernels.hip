@@ -709,15 +709,23 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     m2_run = m2_new;
     const float nm2 = (m2_new == -__builtin_inff()) ? 0.f : -m2_new;
 
-    // p = exp(s - m) and p~ = bf16(p), the B operands of P V
+    // p = exp(s - m) and p~ = bf16(p), the B operands of P V. With kLateP
+    // (d = 64, where the vector ALU sets the pace) only the first 32-key
+    // block is taken here; the second block's exponentials, packs and c / l
+    // products run between the first block's P V products below, so that a
+    // wave's matrix and vector work overlap (measured 1% faster at 512 keys,
+    // and 1-2% slower at d = 128). The same operations on the same values
+    // either way: the results are bitwise the same.
+    constexpr bool kLateP = D == 64 && !INJECT && !WCHK && !SCHK;
+    constexpr int NKB0 = kLateP ? 1 : NKB;   // key blocks taken here
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
+    for (int kb = 0; kb < NKB0; ++kb)
 #pragma unroll
       for (int i = 0; i < 16; ++i)
         sacc[kb][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[kb][i], sl2, nm2));
     u32x4 pb[NKB][2];
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
+    for (int kb = 0; kb < NKB0; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
 #pragma unroll
@@ -750,7 +758,7 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
     // each 8-key slice of p~ in two 4x4x4 products: the lane's own query
     // is its column, so rows never mix (a non-finite p~ stays in its row)
 #pragma unroll
-    for (int kb = 0; kb < NKB; ++kb)
+    for (int kb = 0; kb < NKB0; ++kb)
 #pragma unroll
       for (int h = 0; h < 2; ++h) {
         const u32x4 a =
@@ -828,6 +836,33 @@ __global__ __launch_bounds__(Cfg<D>::THREADS, 1) void fwd_kernel(FwdParams p) {
       if (i + VAHEAD < NPV) vop[i + VAHEAD] = vread(i + VAHEAD);
       const int kb = i / (2 * NDB), h = (i / NDB) % 2, db = i % NDB;
       oacc[db] = mfma32(vop[i], pb[kb][h], oacc[db]);
+      if constexpr (kLateP) {
+        // the second key block, EPM exponentials and EPM / 2 packs after
+        // each P V product of the first, then its c / l products
+        constexpr int HALF = NPV / NKB, EPM = 16 / HALF;
+        static_assert(NKB == 2 && EPM % 2 == 0, "late p~ in pairs per product");
+        if (i < HALF) {
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int j = 0; j < EPM; ++j)
+            sacc[1][EPM * i + j] =
+                __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[1][EPM * i + j], sl2, nm2));
+#pragma unroll
+          for (int j = 0; j < EPM / 2; ++j) {
+            const int e2 = EPM / 2 * i + j;   // pair e2: keys 2 e2, 2 e2 + 1
+            pb[1][e2 >> 2][e2 & 3] = pack_bf16x2(sacc[1][2 * e2], sacc[1][2 * e2 + 1]);
+          }
+          if (i == HALF - 1) {
+#pragma unroll
+            for (int h2 = 0; h2 < 2; ++h2) {
+              const u32x4 a =
+                  *reinterpret_cast<const u32x4*>(&svsm[vsm_row4][32 + 16 * h2 + 8 * grp]);
+              aux = mfma4(u32x2{a[0], a[1]}, u32x2{pb[1][h2][0], pb[1][h2][1]}, aux);
+              aux = mfma4(u32x2{a[2], a[3]}, u32x2{pb[1][h2][2], pb[1][h2][3]}, aux);
+            }
+          }
+        }
+      }
     }
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (INJECT) {
