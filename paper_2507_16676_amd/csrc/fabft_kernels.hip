@@ -32,8 +32,8 @@
 //    so that the S^T accumulator of a lane already holds, for each 16-key
 //    step of P V, the 8 consecutive keys its B operand needs.
 //  * sumrow(V) of a key tile is computed from LDS by the workgroup (four
-//    threads per key; at d = 128 on waves 0-3 only, one per SIMD; fp32 via
-//    v_dot2 and a DPP reduction) while the tile before it is processed,
+//    threads per key on waves 0-3, one per SIMD; fp32 via v_dot2 and a DPP
+//    reduction) while the tile before it is processed,
 //    and stored as a bf16 pair
 //    hi + lo (hi = bf16(vs), lo = bf16(vs - hi); |vs - hi - lo| <=
 //    2^-17|vs|) in an 8-row operand [sumrow hi; sumrow lo; ones; 0; weighted
@@ -79,7 +79,7 @@
 // This file is compiled twice. Part 0 holds everything except the d = 128
 // forward kernels without the weighted check; part 1 holds only those and
 // is built with LLVM's iterative ILP scheduler, measured 2-3% faster for
-// them (and 2.5% slower at d = 64, which therefore stays in part 0). A
+// them (and 2-4% slower at d = 64, which therefore stays in part 0). A
 // kernel is instantiated in one part only.
 #ifndef FABFT_PART
 #define FABFT_PART 0
