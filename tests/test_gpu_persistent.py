@@ -18,8 +18,8 @@ pytestmark = pytest.mark.gpu
 
 F = pytest.importorskip("paper_2507_16676_amd")
 
-# name, B, H, Lq, Lk, d, causal: all but the last have more items than one
-# workgroup per CU (two at d = 64) can hold
+# name, B, H, Lq, Lk, d, causal: all have more items than one workgroup per
+# CU can hold
 CASES = [
     ("causal_d128", 2, 16, 4096, 4096, 128, True),      # every item passes its ring on
     ("causal_d96", 4, 8, 4000, 4000, 96, True),         # each head's last item is ragged
@@ -29,6 +29,7 @@ CASES = [
     ("full_d128", 4, 24, 3000, 1024, 128, False),
     ("bert_d64", 32, 12, 512, 512, 64, False),
     ("causal_d64", 4, 16, 2048, 2048, 64, True),
+    ("full_d64_ragged", 8, 16, 1000, 700, 64, False),   # 11 tiles: never passed on
     ("causal_odd_heads", 3, 7, 2048, 2048, 128, True),  # B*H not a multiple of 8
 ]
 
